@@ -1,0 +1,154 @@
+/*
+ * aflex.h -- C ABI of the decode-step Attention / FFN operator library for
+ * AMD Instinct MI355X (gfx950).
+ *
+ * The paper (AFlex, "Energy-Efficient LLM Serving via Disaggregated
+ * Attention-FFN and Flexible Frequency Scaling") disaggregates each decode
+ * layer into an Attention stage (DA) and an FFN stage (DF) that exchange the
+ * hidden states [tokens, hidden] at every layer boundary (section 4.3, "AFD
+ * Data Plane") and runs them as an interleaved microbatch pipeline whose
+ * timing Eq. 2 models. This library provides the two operators and that
+ * pipeline on one GPU:
+ *
+ *   aflex_attn_decode       batched GQA decode attention over a paged KV cache
+ *   aflex_ffn_swiglu        dense SwiGLU FFN (Qwen3-32B-shaped layers)
+ *   aflex_moe_ffn           top-k mixture-of-experts SwiGLU FFN (Mixtral-8x7B)
+ *   aflex_af_pipeline_step  M microbatches of A then F on two HIP streams
+ *
+ * Conventions shared by every entry point
+ *  - bf16 tensors are passed as raw bit patterns (aflex_bf16 = uint16_t).
+ *  - All tensor pointers are DEVICE pointers owned by the caller, dense
+ *    row-major in the layout stated, 16-byte aligned. Inputs are read-only;
+ *    outputs must not alias inputs.
+ *  - Every call is asynchronous on the given stream(s) (an aflex_stream is a
+ *    hipStream_t; NULL is the null stream). Nothing on the hot path allocates
+ *    or synchronises with the host; the caller passes a device workspace of at
+ *    least the size the matching *_workspace query returns, 256-byte aligned.
+ *  - Arguments are validated on the host before anything is launched. On a
+ *    non-OK status nothing has been launched and aflex_last_error() returns a
+ *    message. Values that live in device memory (context lengths, block ids,
+ *    logits) cannot be validated on the host; the kernels clamp them so that
+ *    no access leaves the caller's buffers (see each entry point).
+ *  - No function throws or aborts; HIP failures return AFLEX_ERR_HIP.
+ */
+#ifndef AFLEX_H
+#define AFLEX_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef uint16_t aflex_bf16;
+typedef void *aflex_stream;
+
+typedef enum aflex_status {
+  AFLEX_OK = 0,
+  AFLEX_ERR_INVALID_ARG = 1, /* null pointer, non-positive or inconsistent size */
+  AFLEX_ERR_UNSUPPORTED = 2, /* a shape outside what the kernels implement */
+  AFLEX_ERR_ALIGNMENT = 3,   /* a pointer that is not 16-byte aligned */
+  AFLEX_ERR_WORKSPACE = 4,   /* workspace missing or smaller than required */
+  AFLEX_ERR_HIP = 5          /* a HIP runtime call failed (message has details) */
+} aflex_status;
+
+/* ------------------------------------------------------------------------ */
+/* Decode attention (DA). The decode step's attention reads the whole cached  */
+/* context of every sequence (section 1; section 2, "LLM Serving"). For each  */
+/* sequence b < B and query head h < Hq, with G = Hq / Hkv and g = h / G:     */
+/*   k_j = k_cache[block_table[b][j / bs]][g][j % bs][:]      j < ctx_b       */
+/*   v_j = v_cache[block_table[b][j / bs]][g][:][j % bs]                      */
+/*   out[b][h] = sum_j softmax_j(scale * <q[b][h], k_j>) * v_j   (bf16)       */
+/* ------------------------------------------------------------------------ */
+typedef struct aflex_attn_args {
+  const aflex_bf16 *q;         /* [B, Hq, D] */
+  const aflex_bf16 *k_cache;   /* [num_blocks, Hkv, block_size, D] */
+  const aflex_bf16 *v_cache;   /* [num_blocks, Hkv, D, block_size]  (token fastest) */
+  const int32_t *block_table;  /* [B, max_blocks_per_seq]; entries >= ceil(ctx/bs) unread */
+  const int32_t *context_lens; /* [B]; valid cached tokens incl. the current one */
+  aflex_bf16 *out;             /* [B, Hq, D] */
+  int32_t B, Hq, Hkv, D;
+  int32_t block_size;          /* must be 16 */
+  int32_t max_blocks_per_seq;  /* row stride of block_table */
+  int32_t num_blocks;          /* blocks in each pool; ids outside [0, num_blocks) are skipped */
+  int32_t max_context_len;     /* host-known bound on every ctx_b (<= max_blocks_per_seq*bs);
+                                  sizes the launch grid, larger device values are clamped */
+  float scale;                 /* softmax scale; 0 selects 1/sqrt(D) */
+  int32_t split_tokens;        /* tokens per work-group split; 0 selects the library default,
+                                  else a multiple of 128 in [128, 1024] */
+} aflex_attn_args;
+
+/* Supported: D in {64, 128}, block_size == 16, Hkv >= 1, Hq % Hkv == 0,
+ * 1 <= Hq / Hkv <= 16. ctx_b == 0 yields out = 0. Block ids outside
+ * [0, num_blocks) contribute nothing (their tokens are masked). */
+aflex_status aflex_attn_decode_workspace(const aflex_attn_args *a, size_t *bytes);
+aflex_status aflex_attn_decode(const aflex_attn_args *a, void *workspace, size_t workspace_bytes,
+                               aflex_stream stream);
+
+/* ------------------------------------------------------------------------ */
+/* FFN (DF). Dense SwiGLU, the FFN of the dense model the paper evaluates     */
+/* (Qwen3-32B, section 6.1), memory-bound at small decode batches and         */
+/* compute-bound at large ones (section 1):                                   */
+/*   y = (SiLU(x W_g^T) * (x W_u^T)) W_d^T,   SiLU(z) = z / (1 + exp(-z))    */
+/* MoE: top-k of E SwiGLU experts (Mixtral-8x7B, section 6.1, section 6.2),   */
+/*   ids_t = top-k experts by router logit (ties -> lower id),                */
+/*   w_t   = softmax over the k selected logits,                              */
+/*   y_t   = sum_j w_t,j * SwiGLU_{ids_t,j}(x_t).                             */
+/* ------------------------------------------------------------------------ */
+typedef struct aflex_ffn_args {
+  const aflex_bf16 *x;          /* [T, H] */
+  const float *router_logits;   /* [T, E] fp32 (MoE only; must be finite) */
+  const aflex_bf16 *w_gate;     /* dense [I, H]; MoE [E, I, H] */
+  const aflex_bf16 *w_up;       /* dense [I, H]; MoE [E, I, H] */
+  const aflex_bf16 *w_down;     /* dense [H, I]; MoE [E, H, I] */
+  aflex_bf16 *y;                /* [T, H] */
+  int32_t *topk_ids;            /* MoE optional output [T, k] (NULL: not written) */
+  float *topk_w;                /* MoE optional output [T, k] */
+  int32_t *expert_offsets;      /* MoE optional output [E + 1]: exclusive prefix of counts */
+  int32_t *sorted_pairs;        /* MoE optional output [T * k]: pair ids t*k+j ordered by
+                                   (expert, token, slot) */
+  int32_t T, H, I;
+  int32_t E, k;                 /* MoE only: experts and experts per token (ignored by dense) */
+} aflex_ffn_args;
+
+/* Supported: H and I multiples of 64, T >= 1; MoE 1 <= k <= E <= 64. */
+aflex_status aflex_ffn_swiglu_workspace(const aflex_ffn_args *f, size_t *bytes);
+aflex_status aflex_ffn_swiglu(const aflex_ffn_args *f, void *workspace, size_t workspace_bytes,
+                              aflex_stream stream);
+aflex_status aflex_moe_ffn_workspace(const aflex_ffn_args *f, size_t *bytes);
+aflex_status aflex_moe_ffn(const aflex_ffn_args *f, void *workspace, size_t workspace_bytes,
+                           aflex_stream stream);
+
+/* ------------------------------------------------------------------------ */
+/* Interleaved A/F layer step (section 4.3, "Interleaved A/F Pipeline"; Eq. 2)*/
+/* The batch is cut into M contiguous microbatches of host-known sizes        */
+/* mb_sizes[0..M) (sum = B). Attention of microbatch i runs on stream_a, its  */
+/* FFN on stream_f once that attention is done; A of layer step l+1 for       */
+/* microbatch i starts as soon as F of step l for i is done, so A of one      */
+/* microbatch overlaps F of another. The FFN input is the attention output    */
+/* viewed as [n_i, Hq*D] (so ffn->H must equal Hq*D); for L > 1 the FFN       */
+/* output viewed as [n_i, Hq, D] is the next step's q. ffn->E == 0 selects    */
+/* the dense SwiGLU, else the MoE with router logits rows of microbatch i.    */
+/* attn->q is the first step's q, attn->out is unused (may be NULL),          */
+/* ffn->x is unused (may be NULL), ffn->y [B, H] receives the last step's     */
+/* output and the optional MoE outputs are not written. On return stream_f    */
+/* is ordered after all of the step's work on both streams.                   */
+/* ------------------------------------------------------------------------ */
+aflex_status aflex_af_pipeline_workspace(const aflex_attn_args *attn, const aflex_ffn_args *ffn,
+                                         int32_t M, const int32_t *mb_sizes, int32_t L,
+                                         size_t *bytes);
+aflex_status aflex_af_pipeline_step(const aflex_attn_args *attn, const aflex_ffn_args *ffn,
+                                    int32_t M, const int32_t *mb_sizes, int32_t L,
+                                    void *workspace, size_t workspace_bytes,
+                                    aflex_stream stream_a, aflex_stream stream_f);
+
+/* Thread-local message describing the last non-OK status of this thread. */
+const char *aflex_last_error(void);
+/* Library version string. */
+const char *aflex_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* AFLEX_H */

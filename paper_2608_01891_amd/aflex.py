@@ -1,0 +1,230 @@
+"""Python binding of libaflex.so (ctypes; argument marshalling only).
+
+Every computation runs in the library's HIP kernels; this module only turns
+torch device tensors into pointers and sizes, sizes the workspace, and maps
+status codes to exceptions. It never falls back to another implementation:
+if the library is not built or no GPU is present, calls raise.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libaflex.so")
+HEADER = os.path.join(os.path.dirname(_PKG), "include", "aflex.h")
+
+OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_ALIGNMENT, ERR_WORKSPACE, ERR_HIP = range(6)
+
+_p = ctypes.c_void_p
+_i = ctypes.c_int32
+
+
+class AttnArgs(ctypes.Structure):
+    _fields_ = [("q", _p), ("k_cache", _p), ("v_cache", _p), ("block_table", _p),
+                ("context_lens", _p), ("out", _p),
+                ("B", _i), ("Hq", _i), ("Hkv", _i), ("D", _i), ("block_size", _i),
+                ("max_blocks_per_seq", _i), ("num_blocks", _i), ("max_context_len", _i),
+                ("scale", ctypes.c_float), ("split_tokens", _i)]
+
+
+class FfnArgs(ctypes.Structure):
+    _fields_ = [("x", _p), ("router_logits", _p), ("w_gate", _p), ("w_up", _p), ("w_down", _p),
+                ("y", _p), ("topk_ids", _p), ("topk_w", _p), ("expert_offsets", _p),
+                ("sorted_pairs", _p),
+                ("T", _i), ("H", _i), ("I", _i), ("E", _i), ("k", _i)]
+
+
+class AflexError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"aflex status {status}: {message}")
+        self.status = status
+
+
+_lib = None
+_SZ = ctypes.POINTER(ctypes.c_size_t)
+
+
+def exported_names():
+    """Function names declared in include/aflex.h."""
+    with open(HEADER) as f:
+        text = f.read()
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\s*\*?\s*(aflex_\w+)\s*\(", text, re.M)))
+
+
+def load():
+    """Open the built library (cached). Raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is missing: build it with `python -m paper_2608_01891_amd.build`")
+    lib = ctypes.CDLL(LIB_PATH)
+    AP, FP = ctypes.POINTER(AttnArgs), ctypes.POINTER(FfnArgs)
+    I32P = ctypes.POINTER(ctypes.c_int32)
+    sig = {
+        "aflex_attn_decode_workspace": [AP, _SZ],
+        "aflex_attn_decode": [AP, _p, ctypes.c_size_t, _p],
+        "aflex_ffn_swiglu_workspace": [FP, _SZ],
+        "aflex_ffn_swiglu": [FP, _p, ctypes.c_size_t, _p],
+        "aflex_moe_ffn_workspace": [FP, _SZ],
+        "aflex_moe_ffn": [FP, _p, ctypes.c_size_t, _p],
+        "aflex_af_pipeline_workspace": [AP, FP, _i, I32P, _i, _SZ],
+        "aflex_af_pipeline_step": [AP, FP, _i, I32P, _i, _p, ctypes.c_size_t, _p, _p],
+    }
+    for name, args in sig.items():
+        fn = getattr(lib, name)
+        fn.argtypes = args
+        fn.restype = ctypes.c_int
+    lib.aflex_last_error.restype = ctypes.c_char_p
+    lib.aflex_version.restype = ctypes.c_char_p
+    _lib = lib
+    return lib
+
+
+def _check(status: int):
+    if status != OK:
+        raise AflexError(status, _lib.aflex_last_error().decode())
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(s):
+    if s is None:
+        s = torch.cuda.current_stream()
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+class Workspace:
+    """Grow-only device scratch handed to the library (allocated by torch)."""
+
+    def __init__(self, device=None):
+        self.device = device
+        self.buf = None
+
+    def get(self, nbytes: int, device):
+        if self.buf is None or self.buf.numel() < nbytes or self.buf.device != torch.device(device):
+            self.buf = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=device)
+        return self.buf
+
+
+_default_ws = {}
+
+
+def _ws(key, nbytes, device, ws):
+    if ws is None:
+        ws = _default_ws.setdefault(key, Workspace())
+    buf = ws.get(nbytes, device)
+    return ctypes.c_void_p(buf.data_ptr()), ctypes.c_size_t(buf.numel())
+
+
+# --------------------------------------------------------------------------
+def attn_args(a, out=None, split_tokens: int = 0, scale: float = 0.0) -> AttnArgs:
+    """Argument block from synth.AttnInputs-like attributes (device tensors)."""
+    return AttnArgs(q=_ptr(a.q), k_cache=_ptr(a.k_cache), v_cache=_ptr(a.v_cache),
+                    block_table=_ptr(a.block_table), context_lens=_ptr(a.context_lens),
+                    out=_ptr(out), B=a.B, Hq=a.Hq, Hkv=a.Hkv, D=a.D, block_size=a.block_size,
+                    max_blocks_per_seq=a.max_blocks, num_blocks=a.num_blocks,
+                    max_context_len=a.max_context_len, scale=scale, split_tokens=split_tokens)
+
+
+def ffn_args(x, w, y, logits=None, k: int = 0, routing=None) -> FfnArgs:
+    T = (x.shape[0] if x is not None else y.shape[0])
+    r = routing or {}
+    return FfnArgs(x=_ptr(x), router_logits=_ptr(logits), w_gate=_ptr(w.w_gate),
+                   w_up=_ptr(w.w_up), w_down=_ptr(w.w_down), y=_ptr(y),
+                   topk_ids=_ptr(r.get("topk_ids")), topk_w=_ptr(r.get("topk_w")),
+                   expert_offsets=_ptr(r.get("expert_offsets")),
+                   sorted_pairs=_ptr(r.get("sorted_pairs")),
+                   T=T, H=w.H, I=w.I, E=w.E, k=k)
+
+
+def attn_decode(a, out=None, split_tokens: int = 0, scale: float = 0.0, stream=None, ws=None):
+    lib = load()
+    if out is None:
+        out = torch.empty(a.B, a.Hq, a.D, dtype=torch.bfloat16, device=a.q.device)
+    args = attn_args(a, out, split_tokens, scale)
+    n = ctypes.c_size_t()
+    _check(lib.aflex_attn_decode_workspace(ctypes.byref(args), ctypes.byref(n)))
+    p, sz = _ws("attn", n.value, a.q.device, ws)
+    _check(lib.aflex_attn_decode(ctypes.byref(args), p, sz, _stream(stream)))
+    return out
+
+
+def ffn_swiglu(x, w, y=None, stream=None, ws=None):
+    lib = load()
+    if y is None:
+        y = torch.empty(x.shape[0], w.H, dtype=torch.bfloat16, device=x.device)
+    args = ffn_args(x, w, y)
+    n = ctypes.c_size_t()
+    _check(lib.aflex_ffn_swiglu_workspace(ctypes.byref(args), ctypes.byref(n)))
+    p, sz = _ws("ffn", n.value, x.device, ws)
+    _check(lib.aflex_ffn_swiglu(ctypes.byref(args), p, sz, _stream(stream)))
+    return y
+
+
+def moe_ffn(x, w, logits, k: int, y=None, routing: bool = False, stream=None, ws=None):
+    """y [T, H]; with routing=True also the topk ids/weights, offsets and pair order."""
+    lib = load()
+    T = x.shape[0]
+    if y is None:
+        y = torch.empty(T, w.H, dtype=torch.bfloat16, device=x.device)
+    r = None
+    if routing:
+        r = {"topk_ids": torch.empty(T, k, dtype=torch.int32, device=x.device),
+             "topk_w": torch.empty(T, k, dtype=torch.float32, device=x.device),
+             "expert_offsets": torch.empty(w.E + 1, dtype=torch.int32, device=x.device),
+             "sorted_pairs": torch.empty(T * k, dtype=torch.int32, device=x.device)}
+    args = ffn_args(x, w, y, logits, k, r)
+    n = ctypes.c_size_t()
+    _check(lib.aflex_moe_ffn_workspace(ctypes.byref(args), ctypes.byref(n)))
+    p, sz = _ws("moe", n.value, x.device, ws)
+    _check(lib.aflex_moe_ffn(ctypes.byref(args), p, sz, _stream(stream)))
+    return (y, r) if routing else y
+
+
+_pipe_streams = {}
+
+
+def pipeline_streams(device):
+    """A pair of default-priority side streams for the two pipeline stages."""
+    d = torch.device(device)
+    if d not in _pipe_streams:
+        _pipe_streams[d] = (torch.cuda.Stream(device=d), torch.cuda.Stream(device=d))
+    return _pipe_streams[d]
+
+
+def af_pipeline_step(a, w, logits, k: int, mb_sizes, L: int = 1, y=None, stream_a=None,
+                     stream_f=None, ws=None, split_tokens: int = 0, join: bool = True):
+    """Interleaved A/F layer step(s); returns y [B, Hq*D].
+
+    Without explicit streams the step runs on two side streams that first wait
+    for the current stream; with ``join`` the current stream then waits for
+    stream_f, so the result is ordered on the caller's stream.
+    """
+    lib = load()
+    if stream_a is None or stream_f is None:
+        stream_a, stream_f = pipeline_streams(a.q.device)
+        cur = torch.cuda.current_stream(a.q.device)
+        stream_a.wait_stream(cur)
+        stream_f.wait_stream(cur)
+    if y is None:
+        y = torch.empty(a.B, a.Hq * a.D, dtype=torch.bfloat16, device=a.q.device)
+    aa = attn_args(a, None, split_tokens)
+    fa = ffn_args(None, w, y, logits, k)
+    M = len(mb_sizes)
+    mb = (ctypes.c_int32 * M)(*mb_sizes)
+    n = ctypes.c_size_t()
+    _check(lib.aflex_af_pipeline_workspace(ctypes.byref(aa), ctypes.byref(fa), M, mb, L,
+                                           ctypes.byref(n)))
+    p, sz = _ws("pipe", n.value, a.q.device, ws)
+    _check(lib.aflex_af_pipeline_step(ctypes.byref(aa), ctypes.byref(fa), M, mb, L, p, sz,
+                                      _stream(stream_a), _stream(stream_f)))
+    if join:
+        torch.cuda.current_stream(a.q.device).wait_stream(stream_f)
+    return y

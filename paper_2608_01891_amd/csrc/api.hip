@@ -1,0 +1,295 @@
+// C-ABI layer of libaflex: host-side validation, workspace queries, launches
+// and the two-stream interleaved A/F layer-step driver.
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+
+#include <mutex>
+#include <vector>
+
+#include "aflex.h"
+#include "kernels.h"
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+aflex_status fail(aflex_status s, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof(g_err), fmt, ap);
+  va_end(ap);
+  return s;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+#define REQUIRE(cond, status, ...) \
+  do {                             \
+    if (!(cond)) return fail(status, __VA_ARGS__); \
+  } while (0)
+
+aflex_status check_attn(const aflex_attn_args* a, bool need_out) {
+  REQUIRE(a, AFLEX_ERR_INVALID_ARG, "attn: args is NULL");
+  REQUIRE(a->q && a->k_cache && a->v_cache && a->block_table && a->context_lens, AFLEX_ERR_INVALID_ARG,
+          "attn: NULL tensor pointer");
+  REQUIRE(!need_out || a->out, AFLEX_ERR_INVALID_ARG, "attn: out is NULL");
+  REQUIRE(a->B >= 1 && a->Hq >= 1 && a->Hkv >= 1 && a->D >= 1, AFLEX_ERR_INVALID_ARG,
+          "attn: B, Hq, Hkv, D must be positive (got %d, %d, %d, %d)", a->B, a->Hq, a->Hkv, a->D);
+  REQUIRE(a->num_blocks >= 1 && a->max_blocks_per_seq >= 1, AFLEX_ERR_INVALID_ARG,
+          "attn: num_blocks and max_blocks_per_seq must be positive");
+  REQUIRE(a->max_context_len >= 0, AFLEX_ERR_INVALID_ARG, "attn: max_context_len < 0");
+  REQUIRE(a->Hq % a->Hkv == 0, AFLEX_ERR_INVALID_ARG, "attn: Hq (%d) not a multiple of Hkv (%d)", a->Hq, a->Hkv);
+  REQUIRE(a->D == 64 || a->D == 128, AFLEX_ERR_UNSUPPORTED, "attn: head_dim %d unsupported (64 or 128)", a->D);
+  REQUIRE(a->block_size == 16, AFLEX_ERR_UNSUPPORTED, "attn: block_size %d unsupported (16)", a->block_size);
+  REQUIRE(a->Hq / a->Hkv <= 16, AFLEX_ERR_UNSUPPORTED, "attn: %d query heads per kv head (max 16)",
+          a->Hq / a->Hkv);
+  REQUIRE((long long)a->max_context_len <= (long long)a->max_blocks_per_seq * a->block_size,
+          AFLEX_ERR_INVALID_ARG, "attn: max_context_len %d exceeds the block table capacity %lld",
+          a->max_context_len, (long long)a->max_blocks_per_seq * a->block_size);
+  REQUIRE(a->split_tokens == 0 || (a->split_tokens % 128 == 0 && a->split_tokens >= 128 &&
+                                   a->split_tokens <= 1024),
+          AFLEX_ERR_INVALID_ARG, "attn: split_tokens %d must be 0 or a multiple of 128 in [128, 1024]",
+          a->split_tokens);
+  REQUIRE(isfinite(a->scale) && a->scale >= 0.f, AFLEX_ERR_INVALID_ARG, "attn: scale must be finite and >= 0");
+  REQUIRE(aligned16(a->q) && aligned16(a->k_cache) && aligned16(a->v_cache) && (!a->out || aligned16(a->out)),
+          AFLEX_ERR_ALIGNMENT, "attn: q, k_cache, v_cache and out must be 16-byte aligned");
+  REQUIRE(((uintptr_t)a->block_table & 3u) == 0 && ((uintptr_t)a->context_lens & 3u) == 0, AFLEX_ERR_ALIGNMENT,
+          "attn: block_table and context_lens must be 4-byte aligned");
+  return AFLEX_OK;
+}
+
+aflex_status check_ffn(const aflex_ffn_args* f, bool moe, bool need_x) {
+  const char* who = moe ? "moe" : "swiglu";
+  REQUIRE(f, AFLEX_ERR_INVALID_ARG, "%s: args is NULL", who);
+  REQUIRE((!need_x || f->x) && f->w_gate && f->w_up && f->w_down && f->y, AFLEX_ERR_INVALID_ARG,
+          "%s: NULL tensor pointer", who);
+  REQUIRE(f->T >= 1 && f->H >= 1 && f->I >= 1, AFLEX_ERR_INVALID_ARG, "%s: T, H, I must be positive", who);
+  REQUIRE(f->H % 64 == 0 && f->I % 64 == 0, AFLEX_ERR_UNSUPPORTED, "%s: H (%d) and I (%d) must be multiples of 64",
+          who, f->H, f->I);
+  REQUIRE((!f->x || aligned16(f->x)) && aligned16(f->w_gate) && aligned16(f->w_up) && aligned16(f->w_down) &&
+              aligned16(f->y),
+          AFLEX_ERR_ALIGNMENT, "%s: tensors must be 16-byte aligned", who);
+  if (moe) {
+    REQUIRE(f->router_logits, AFLEX_ERR_INVALID_ARG, "moe: router_logits is NULL");
+    REQUIRE(f->E >= 1 && f->k >= 1 && f->k <= f->E, AFLEX_ERR_INVALID_ARG, "moe: need 1 <= k <= E (k=%d, E=%d)",
+            f->k, f->E);
+    REQUIRE(f->E <= 64 && f->k <= 8, AFLEX_ERR_UNSUPPORTED, "moe: E <= 64 and k <= 8 supported (E=%d, k=%d)", f->E,
+            f->k);
+    REQUIRE((long long)f->T * f->k < (1ll << 30), AFLEX_ERR_UNSUPPORTED, "moe: too many token/slot pairs");
+  }
+  return AFLEX_OK;
+}
+
+aflex_status check_ws(void* ws, size_t have, size_t need, const char* who) {
+  REQUIRE(have >= need, AFLEX_ERR_WORKSPACE, "%s: workspace of %zu bytes, %zu required", who, have, need);
+  REQUIRE(need == 0 || ws, AFLEX_ERR_WORKSPACE, "%s: workspace is NULL", who);
+  REQUIRE(((uintptr_t)ws & 255u) == 0, AFLEX_ERR_ALIGNMENT, "%s: workspace must be 256-byte aligned", who);
+  return AFLEX_OK;
+}
+
+aflex_status hip_status(hipError_t e, const char* who) {
+  if (e == hipSuccess) return AFLEX_OK;
+  return fail(AFLEX_ERR_HIP, "%s: HIP error %d (%s)", who, (int)e, hipGetErrorString(e));
+}
+
+// ---------------------------------------------------------------------------
+// Pipeline driver.
+struct PipeLayout {
+  size_t attn_out, attn_ws, ffn_ws, total;
+};
+
+aflex_attn_args mb_attn(const aflex_attn_args& a, int off, int n) {
+  aflex_attn_args m = a;
+  m.B = n;
+  m.q = a.q + (size_t)off * a.Hq * a.D;
+  m.block_table = a.block_table + (size_t)off * a.max_blocks_per_seq;
+  m.context_lens = a.context_lens + off;
+  m.out = a.out ? a.out + (size_t)off * a.Hq * a.D : nullptr;
+  return m;
+}
+
+aflex_ffn_args mb_ffn(const aflex_ffn_args& f, int off, int n) {
+  aflex_ffn_args m = f;
+  m.T = n;
+  m.x = f.x ? f.x + (size_t)off * f.H : nullptr;
+  m.y = f.y + (size_t)off * f.H;
+  m.router_logits = f.router_logits ? f.router_logits + (size_t)off * f.E : nullptr;
+  m.topk_ids = nullptr;
+  m.topk_w = nullptr;
+  m.expert_offsets = nullptr;
+  m.sorted_pairs = nullptr;
+  return m;
+}
+
+PipeLayout pipe_layout(const aflex_attn_args& a, const aflex_ffn_args& f, int M, const int32_t* mb) {
+  PipeLayout L;
+  size_t aw = 0, fw = 0;
+  int off = 0;
+  for (int i = 0; i < M; ++i) {
+    aflex_attn_args am = mb_attn(a, off, mb[i]);
+    aflex_ffn_args fm = mb_ffn(f, off, mb[i]);
+    size_t x = aflex::attn_workspace_bytes(am);
+    size_t y = f.E ? aflex::moe_workspace_bytes(fm) : aflex::swiglu_workspace_bytes(fm);
+    aw = x > aw ? x : aw;
+    fw = y > fw ? y : fw;
+    off += mb[i];
+  }
+  L.attn_out = 0;
+  L.attn_ws = aflex::align_up((size_t)a.B * a.Hq * a.D * 2, 256);
+  L.ffn_ws = L.attn_ws + aflex::align_up(aw, 256);
+  L.total = L.ffn_ws + aflex::align_up(fw, 256);
+  return L;
+}
+
+aflex_status check_pipe(const aflex_attn_args* a, const aflex_ffn_args* f, int32_t M, const int32_t* mb, int32_t L) {
+  aflex_status s = check_attn(a, false);
+  if (s != AFLEX_OK) return s;
+  s = check_ffn(f, f && f->E > 0, false);
+  if (s != AFLEX_OK) return s;
+  REQUIRE(M >= 1 && M <= 64, AFLEX_ERR_INVALID_ARG, "pipeline: M=%d must be in [1, 64]", M);
+  REQUIRE(mb, AFLEX_ERR_INVALID_ARG, "pipeline: mb_sizes is NULL");
+  REQUIRE(L >= 1, AFLEX_ERR_INVALID_ARG, "pipeline: L=%d must be >= 1", L);
+  long long sum = 0;
+  for (int i = 0; i < M; ++i) {
+    REQUIRE(mb[i] >= 1, AFLEX_ERR_INVALID_ARG, "pipeline: mb_sizes[%d]=%d must be >= 1", i, mb[i]);
+    sum += mb[i];
+  }
+  REQUIRE(sum == a->B, AFLEX_ERR_INVALID_ARG, "pipeline: sum of mb_sizes %lld != B %d", sum, a->B);
+  REQUIRE(f->T == a->B, AFLEX_ERR_INVALID_ARG, "pipeline: ffn T %d != attention B %d", f->T, a->B);
+  REQUIRE(f->H == a->Hq * a->D, AFLEX_ERR_INVALID_ARG, "pipeline: ffn H %d != Hq*D %d", f->H, a->Hq * a->D);
+  return AFLEX_OK;
+}
+
+struct EventPool {
+  std::mutex mu;
+  std::vector<std::vector<hipEvent_t>> per_device;
+};
+EventPool g_events;
+
+}  // namespace
+
+extern "C" {
+
+const char* aflex_last_error(void) { return g_err; }
+const char* aflex_version(void) { return "aflex 0.1 gfx950"; }
+
+aflex_status aflex_attn_decode_workspace(const aflex_attn_args* a, size_t* bytes) {
+  REQUIRE(bytes, AFLEX_ERR_INVALID_ARG, "attn: bytes is NULL");
+  aflex_status s = check_attn(a, false);
+  if (s != AFLEX_OK) return s;
+  *bytes = aflex::attn_workspace_bytes(*a);
+  return AFLEX_OK;
+}
+
+aflex_status aflex_attn_decode(const aflex_attn_args* a, void* ws, size_t ws_bytes, aflex_stream stream) {
+  aflex_status s = check_attn(a, true);
+  if (s != AFLEX_OK) return s;
+  s = check_ws(ws, ws_bytes, aflex::attn_workspace_bytes(*a), "attn");
+  if (s != AFLEX_OK) return s;
+  return hip_status(aflex::launch_attn_decode(*a, ws, (hipStream_t)stream), "attn");
+}
+
+aflex_status aflex_ffn_swiglu_workspace(const aflex_ffn_args* f, size_t* bytes) {
+  REQUIRE(bytes, AFLEX_ERR_INVALID_ARG, "swiglu: bytes is NULL");
+  aflex_status s = check_ffn(f, false, true);
+  if (s != AFLEX_OK) return s;
+  *bytes = aflex::swiglu_workspace_bytes(*f);
+  return AFLEX_OK;
+}
+
+aflex_status aflex_ffn_swiglu(const aflex_ffn_args* f, void* ws, size_t ws_bytes, aflex_stream stream) {
+  aflex_status s = check_ffn(f, false, true);
+  if (s != AFLEX_OK) return s;
+  s = check_ws(ws, ws_bytes, aflex::swiglu_workspace_bytes(*f), "swiglu");
+  if (s != AFLEX_OK) return s;
+  return hip_status(aflex::launch_swiglu(*f, ws, (hipStream_t)stream), "swiglu");
+}
+
+aflex_status aflex_moe_ffn_workspace(const aflex_ffn_args* f, size_t* bytes) {
+  REQUIRE(bytes, AFLEX_ERR_INVALID_ARG, "moe: bytes is NULL");
+  aflex_status s = check_ffn(f, true, true);
+  if (s != AFLEX_OK) return s;
+  *bytes = aflex::moe_workspace_bytes(*f);
+  return AFLEX_OK;
+}
+
+aflex_status aflex_moe_ffn(const aflex_ffn_args* f, void* ws, size_t ws_bytes, aflex_stream stream) {
+  aflex_status s = check_ffn(f, true, true);
+  if (s != AFLEX_OK) return s;
+  s = check_ws(ws, ws_bytes, aflex::moe_workspace_bytes(*f), "moe");
+  if (s != AFLEX_OK) return s;
+  return hip_status(aflex::launch_moe(*f, ws, (hipStream_t)stream), "moe");
+}
+
+aflex_status aflex_af_pipeline_workspace(const aflex_attn_args* a, const aflex_ffn_args* f, int32_t M,
+                                         const int32_t* mb, int32_t L, size_t* bytes) {
+  REQUIRE(bytes, AFLEX_ERR_INVALID_ARG, "pipeline: bytes is NULL");
+  aflex_status s = check_pipe(a, f, M, mb, L);
+  if (s != AFLEX_OK) return s;
+  *bytes = pipe_layout(*a, *f, M, mb).total;
+  return AFLEX_OK;
+}
+
+aflex_status aflex_af_pipeline_step(const aflex_attn_args* a, const aflex_ffn_args* f, int32_t M,
+                                    const int32_t* mb, int32_t L, void* ws, size_t ws_bytes,
+                                    aflex_stream stream_a, aflex_stream stream_f) {
+  aflex_status s = check_pipe(a, f, M, mb, L);
+  if (s != AFLEX_OK) return s;
+  const PipeLayout P = pipe_layout(*a, *f, M, mb);
+  s = check_ws(ws, ws_bytes, P.total, "pipeline");
+  if (s != AFLEX_OK) return s;
+  REQUIRE(stream_a != stream_f, AFLEX_ERR_INVALID_ARG, "pipeline: stream_a and stream_f must differ");
+
+  hipStream_t sa = (hipStream_t)stream_a, sf = (hipStream_t)stream_f;
+  char* w = static_cast<char*>(ws);
+  uint16_t* attn_out = reinterpret_cast<uint16_t*>(w + P.attn_out);
+  void* attn_ws = w + P.attn_ws;
+  void* ffn_ws = w + P.ffn_ws;
+  const int H = f->H;
+
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_status(e, "pipeline");
+  std::lock_guard<std::mutex> lock(g_events.mu);
+  if ((int)g_events.per_device.size() <= dev) g_events.per_device.resize(dev + 1);
+  std::vector<hipEvent_t>& ev = g_events.per_device[dev];
+  const size_t need = 2 * (size_t)M + 1;
+  while (ev.size() < need) {
+    hipEvent_t x;
+    e = hipEventCreateWithFlags(&x, hipEventDisableTiming);
+    if (e != hipSuccess) return hip_status(e, "pipeline: event create");
+    ev.push_back(x);
+  }
+  hipEvent_t entry = ev[0];
+  hipEvent_t* evA = &ev[1];
+  hipEvent_t* evF = &ev[1 + M];
+
+  // Work still queued on stream_f from an earlier call may read the buffers
+  // the first attention overwrites.
+  if ((e = hipEventRecord(entry, sf)) != hipSuccess) return hip_status(e, "pipeline");
+  if ((e = hipStreamWaitEvent(sa, entry, 0)) != hipSuccess) return hip_status(e, "pipeline");
+
+  for (int l = 0; l < L; ++l) {
+    int off = 0;
+    for (int i = 0; i < M; ++i) {
+      const int n = mb[i];
+      if (l > 0 && (e = hipStreamWaitEvent(sa, evF[i], 0)) != hipSuccess) return hip_status(e, "pipeline");
+      aflex_attn_args am = mb_attn(*a, off, n);
+      if (l > 0) am.q = f->y + (size_t)off * H;
+      am.out = attn_out + (size_t)off * H;
+      if ((e = aflex::launch_attn_decode(am, attn_ws, sa)) != hipSuccess) return hip_status(e, "pipeline: attn");
+      if ((e = hipEventRecord(evA[i], sa)) != hipSuccess) return hip_status(e, "pipeline");
+      if ((e = hipStreamWaitEvent(sf, evA[i], 0)) != hipSuccess) return hip_status(e, "pipeline");
+      aflex_ffn_args fm = mb_ffn(*f, off, n);
+      fm.x = attn_out + (size_t)off * H;
+      e = f->E ? aflex::launch_moe(fm, ffn_ws, sf) : aflex::launch_swiglu(fm, ffn_ws, sf);
+      if (e != hipSuccess) return hip_status(e, "pipeline: ffn");
+      if ((e = hipEventRecord(evF[i], sf)) != hipSuccess) return hip_status(e, "pipeline");
+      off += n;
+    }
+  }
+  return AFLEX_OK;
+}
+
+}  // extern "C"

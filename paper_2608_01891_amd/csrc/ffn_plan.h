@@ -1,0 +1,50 @@
+// Tile and split-K planning shared by the dense and MoE FFN launchers.
+#pragma once
+#include <hip/hip_runtime.h>
+
+#include "gemm.h"
+
+namespace aflex {
+
+constexpr int kGateBN = 64;   // output columns per gate/up tile (x2 weight rows)
+constexpr int kDownBN = 128;  // output columns per down tile
+
+struct FfnPlan {
+  int bm;           // rows per m-tile: 32, 64 or 128
+  int down_splits;  // split-K factor of the down GEMM
+  int down_kps;     // k elements per split (multiple of 64)
+};
+
+inline int pick_bm(double rows_per_tile_group) {
+  if (rows_per_tile_group * 1.3 <= 32) return 32;
+  if (rows_per_tile_group * 1.3 <= 64) return 64;
+  return 128;
+}
+
+// Split K so that the down GEMM has about `target` work-groups, keeping at
+// least `min_steps` 64-wide k-steps per split.
+inline void plan_splits(int base_tiles, int K, int target, int min_steps, int* splits, int* kps) {
+  const int ksteps = K / 64;
+  int s = (target + base_tiles - 1) / base_tiles;
+  int smax = ksteps / min_steps;
+  if (smax < 1) smax = 1;
+  if (s > smax) s = smax;
+  if (s < 1) s = 1;
+  const int steps = (ksteps + s - 1) / s;
+  *splits = (ksteps + steps - 1) / steps;
+  *kps = steps * 64;
+}
+
+inline FfnPlan plan_dense(int T, int H, int I) {
+  FfnPlan pl;
+  pl.bm = T <= 32 ? 32 : (T <= 64 ? 64 : 128);
+  const int mtiles = (T + pl.bm - 1) / pl.bm;
+  const int ntiles = (H + kDownBN - 1) / kDownBN;
+  plan_splits(mtiles * ntiles, I, 512, 8, &pl.down_splits, &pl.down_kps);
+  return pl;
+}
+
+hipError_t launch_gate_up(int bm, const GemmParams& g, hipStream_t stream);
+hipError_t launch_down(int bm, bool f32_partials, const GemmParams& g, hipStream_t stream);
+
+}  // namespace aflex

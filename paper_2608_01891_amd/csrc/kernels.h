@@ -1,0 +1,25 @@
+// Internal launch interface between the C-ABI layer and the kernels.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+
+#include "aflex.h"
+
+namespace aflex {
+
+inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+// Decode attention (attn_decode.hip).
+int attn_split_tokens(const aflex_attn_args& a);
+size_t attn_workspace_bytes(const aflex_attn_args& a);
+hipError_t launch_attn_decode(const aflex_attn_args& a, void* ws, hipStream_t stream);
+
+// Dense SwiGLU FFN (ffn.hip).
+size_t swiglu_workspace_bytes(const aflex_ffn_args& f);
+hipError_t launch_swiglu(const aflex_ffn_args& f, void* ws, hipStream_t stream);
+
+// Top-k MoE FFN (moe.hip).
+size_t moe_workspace_bytes(const aflex_ffn_args& f);
+hipError_t launch_moe(const aflex_ffn_args& f, void* ws, hipStream_t stream);
+
+}  // namespace aflex

@@ -1,0 +1,266 @@
+// Top-k mixture-of-experts SwiGLU FFN, gfx950.
+//
+// The FFN of the MoE model the paper evaluates (Mixtral-8x7B, section 6.1;
+// section 6.2 "Generality" notes that sparse expert execution changes the
+// FFN's computation and communication). Steps, all on the device and without
+// a host synchronisation:
+//   1. route: per token, top-k experts by logit (ties -> lower id) and the
+//      softmax over the k selected logits; per-expert counts, their exclusive
+//      prefix, the stable (expert, token, slot) order of the token/slot pairs,
+//      each pair's position in that order, and the m-tile map of the grouped
+//      GEMMs. One work-group; ranks come from wave ballots, so the order is
+//      deterministic.
+//   2. grouped gate/up GEMM with fused SwiGLU; the A rows are gathered from x
+//      through the pair order (no permuted copy of x is written).
+//   3. grouped down GEMM into fp32 split-K partials, rows in pair order.
+//   4. combine: y_t = sum_j w_t,j * (sum over splits of row pos(t,j)), fixed
+//      order, bf16 out.
+#include "ffn_plan.h"
+#include "gemm.h"
+#include "kernels.h"
+
+namespace aflex {
+
+constexpr int kMaxK = 8;
+constexpr int kMaxE = 64;
+
+struct MoeLayout {
+  size_t ids, wts, offsets, sorted, pos, tile_map, num_tiles, h, P, total;
+  int bm, max_tiles, down_splits, down_kps;
+};
+
+static MoeLayout moe_layout(const aflex_ffn_args& f) {
+  MoeLayout L;
+  const size_t pairs = (size_t)f.T * f.k;
+  L.bm = pick_bm((double)pairs / f.E);
+  L.max_tiles = (int)((pairs + L.bm - 1) / L.bm) + f.E;
+  const int ntiles = (f.H + kDownBN - 1) / kDownBN;
+  plan_splits(L.max_tiles * ntiles, f.I, 512, 16, &L.down_splits, &L.down_kps);
+  size_t o = 0;
+  auto take = [&](size_t bytes) {
+    size_t at = o;
+    o += align_up(bytes, 256);
+    return at;
+  };
+  L.ids = take(pairs * 4);
+  L.wts = take(pairs * 4);
+  L.offsets = take((size_t)(f.E + 1) * 4);
+  L.sorted = take(pairs * 4);
+  L.pos = take(pairs * 4);
+  L.tile_map = take((size_t)L.max_tiles * 3 * 4);
+  L.num_tiles = take(4);
+  L.h = take(pairs * f.I * 2);
+  L.P = take((size_t)L.down_splits * pairs * f.H * 4);
+  L.total = o;
+  return L;
+}
+
+size_t moe_workspace_bytes(const aflex_ffn_args& f) { return moe_layout(f).total; }
+
+__global__ __launch_bounds__(256) void moe_route_kernel(const float* __restrict__ logits, int T, int E, int k,
+                                                        int bm, int32_t* ids, float* wts, int32_t* offsets,
+                                                        int32_t* sorted, int32_t* pos, int32_t* tile_map,
+                                                        int32_t* num_tiles, int32_t* u_ids, float* u_w,
+                                                        int32_t* u_offsets, int32_t* u_sorted) {
+  __shared__ int cnt[kMaxE];
+  __shared__ int off[kMaxE + 1];
+  __shared__ int base[kMaxE];
+  __shared__ int wcnt[4][kMaxE];
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  if (tid < kMaxE) {
+    cnt[tid] = 0;
+    base[tid] = 0;
+  }
+  __syncthreads();
+
+  // 1. top-k and softmax over the selected logits.
+  for (int t = tid; t < T; t += 256) {
+    const float* l = logits + (size_t)t * E;
+    uint64_t taken = 0;
+    float sel[kMaxK];
+    int sid[kMaxK];
+    for (int j = 0; j < k; ++j) {
+      int bi = -1;
+      float bv = 0.f;
+      for (int e = 0; e < E; ++e) {
+        if ((taken >> e) & 1) continue;
+        const float v = l[e];
+        if (bi < 0 || v > bv) {
+          bi = e;
+          bv = v;
+        }
+      }
+      taken |= 1ull << bi;
+      sel[j] = bv;
+      sid[j] = bi;
+    }
+    float z = 0.f, ex[kMaxK];
+    for (int j = 0; j < k; ++j) {
+      ex[j] = expf(sel[j] - sel[0]);
+      z += ex[j];
+    }
+    for (int j = 0; j < k; ++j) {
+      const float w = ex[j] / z;
+      ids[t * k + j] = sid[j];
+      wts[t * k + j] = w;
+      if (u_ids) u_ids[t * k + j] = sid[j];
+      if (u_w) u_w[t * k + j] = w;
+      atomicAdd(&cnt[sid[j]], 1);
+    }
+  }
+  __syncthreads();
+
+  // 2. offsets and the m-tile map.
+  if (tid == 0) {
+    off[0] = 0;
+    for (int e = 0; e < E; ++e) off[e + 1] = off[e] + cnt[e];
+    int nt = 0;
+    for (int e = 0; e < E; ++e)
+      for (int r = off[e]; r < off[e + 1]; r += bm) {
+        tile_map[3 * nt + 0] = e;
+        tile_map[3 * nt + 1] = r;
+        tile_map[3 * nt + 2] = min(r + bm, off[e + 1]);
+        ++nt;
+      }
+    *num_tiles = nt;
+  }
+  __syncthreads();
+  if (tid <= E) {
+    offsets[tid] = off[tid];
+    if (u_offsets) u_offsets[tid] = off[tid];
+  }
+
+  // 3. stable ranks: pairs of expert e are ordered by token (a token holds e
+  //    at most once), chunk by chunk of 256 tokens, wave by wave, lane by lane.
+  const uint64_t lt = (1ull << lane) - 1ull;
+  for (int c0 = 0; c0 < T; c0 += 256) {
+    const int t = c0 + tid;
+    const bool valid = t < T;
+    int my_e[kMaxK], pre[kMaxK];
+    uint64_t mask = 0;
+    for (int j = 0; j < k; ++j) {
+      my_e[j] = valid ? ids[t * k + j] : -1;
+      pre[j] = 0;
+      if (valid) mask |= 1ull << my_e[j];
+    }
+    for (int e = 0; e < E; ++e) {
+      const bool f = (mask >> e) & 1ull;
+      const uint64_t bal = __ballot(f);
+      if (f) {
+        const int pr = __popcll(bal & lt);
+        for (int j = 0; j < k; ++j)
+          if (my_e[j] == e) pre[j] = pr;
+      }
+      if (lane == 0) wcnt[wave][e] = __popcll(bal);
+    }
+    __syncthreads();
+    if (valid) {
+      for (int j = 0; j < k; ++j) {
+        const int e = my_e[j];
+        int r = base[e] + pre[j];
+        for (int w = 0; w < wave; ++w) r += wcnt[w][e];
+        const int pidx = off[e] + r;
+        sorted[pidx] = t * k + j;
+        pos[t * k + j] = pidx;
+        if (u_sorted) u_sorted[pidx] = t * k + j;
+      }
+    }
+    __syncthreads();
+    if (tid < E) base[tid] += wcnt[0][tid] + wcnt[1][tid] + wcnt[2][tid] + wcnt[3][tid];
+    __syncthreads();
+  }
+}
+
+__global__ __launch_bounds__(256) void moe_combine_kernel(const float* __restrict__ P, long long split_stride,
+                                                          int splits, const int32_t* __restrict__ pos,
+                                                          const float* __restrict__ w, int k, int H,
+                                                          uint16_t* __restrict__ y) {
+  const int t = blockIdx.x;
+  const int c = (blockIdx.y * 256 + threadIdx.x) * 4;
+  if (c >= H) return;
+  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+  for (int j = 0; j < k; ++j) {
+    const long long row = pos[t * k + j];
+    const float wt = w[t * k + j];
+    f32x4 s = *reinterpret_cast<const f32x4*>(P + row * H + c);
+    for (int sp = 1; sp < splits; ++sp) s += *reinterpret_cast<const f32x4*>(P + sp * split_stride + row * H + c);
+    acc += wt * s;
+  }
+  ushort4 o;
+  o.x = f2bf(acc[0]);
+  o.y = f2bf(acc[1]);
+  o.z = f2bf(acc[2]);
+  o.w = f2bf(acc[3]);
+  *reinterpret_cast<ushort4*>(y + (size_t)t * H + c) = o;
+}
+
+hipError_t launch_moe(const aflex_ffn_args& f, void* ws, hipStream_t stream) {
+  const MoeLayout L = moe_layout(f);
+  char* w = static_cast<char*>(ws);
+  int32_t* ids = reinterpret_cast<int32_t*>(w + L.ids);
+  float* wts = reinterpret_cast<float*>(w + L.wts);
+  int32_t* offsets = reinterpret_cast<int32_t*>(w + L.offsets);
+  int32_t* sorted = reinterpret_cast<int32_t*>(w + L.sorted);
+  int32_t* pos = reinterpret_cast<int32_t*>(w + L.pos);
+  int32_t* tile_map = reinterpret_cast<int32_t*>(w + L.tile_map);
+  int32_t* num_tiles = reinterpret_cast<int32_t*>(w + L.num_tiles);
+  uint16_t* h = reinterpret_cast<uint16_t*>(w + L.h);
+  float* P = reinterpret_cast<float*>(w + L.P);
+
+  moe_route_kernel<<<1, 256, 0, stream>>>(f.router_logits, f.T, f.E, f.k, L.bm, ids, wts, offsets, sorted, pos,
+                                          tile_map, num_tiles, f.topk_ids, f.topk_w, f.expert_offsets,
+                                          f.sorted_pairs);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+
+  GemmParams g = {};
+  g.A = f.x;
+  g.lda = f.H;
+  g.gather = sorted;
+  g.gather_div = f.k;
+  g.B0 = f.w_gate;
+  g.B1 = f.w_up;
+  g.ldb = f.H;
+  g.b_expert_stride = (long long)f.I * f.H;
+  g.N = f.I;
+  g.K = f.H;
+  g.k_per_split = f.H;
+  g.splits = 1;
+  g.tile_map = tile_map;
+  g.num_mtiles = num_tiles;
+  g.max_mtiles = L.max_tiles;
+  g.n_ntiles = (f.I + kGateBN - 1) / kGateBN;
+  g.mt_major = 1;
+  g.C = h;
+  g.ldc = f.I;
+  e = launch_gate_up(L.bm, g, stream);
+  if (e != hipSuccess) return e;
+
+  const long long pairs = (long long)f.T * f.k;
+  GemmParams d = {};
+  d.A = h;
+  d.lda = f.I;
+  d.B0 = f.w_down;
+  d.ldb = f.I;
+  d.b_expert_stride = (long long)f.H * f.I;
+  d.N = f.H;
+  d.K = f.I;
+  d.k_per_split = L.down_kps;
+  d.splits = L.down_splits;
+  d.tile_map = tile_map;
+  d.num_mtiles = num_tiles;
+  d.max_mtiles = L.max_tiles;
+  d.n_ntiles = (f.H + kDownBN - 1) / kDownBN;
+  d.mt_major = 1;
+  d.P = P;
+  d.p_split_stride = pairs * f.H;
+  d.ldp = f.H;
+  e = launch_down(L.bm, true, d, stream);
+  if (e != hipSuccess) return e;
+
+  dim3 grid(f.T, (f.H / 4 + 255) / 256);
+  moe_combine_kernel<<<grid, 256, 0, stream>>>(P, d.p_split_stride, L.down_splits, pos, wts, f.k, f.H, f.y);
+  return hipGetLastError();
+}
+
+}  // namespace aflex

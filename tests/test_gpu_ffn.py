@@ -1,0 +1,44 @@
+"""HIP dense SwiGLU FFN vs the oracle (through the C ABI)."""
+import pytest
+import torch
+
+import oracle
+from paper_2608_01891_amd import aflex, synth
+from tests.helpers import sample_rows
+from tests.parity import check_rows
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda:0"
+
+
+def test_tiny_layer(gpu_lib):
+    w = synth.tiny_layer()
+    y = aflex.ffn_swiglu(w.x.to(DEV), w.ffn.to(DEV)).cpu()
+    check_rows(y, oracle.swiglu_ffn(w.x, w.ffn.w_gate, w.ffn.w_up, w.ffn.w_down), what="tiny swiglu")
+
+
+@pytest.mark.parametrize("T,H,I", [(1, 256, 320), (33, 320, 192), (200, 192, 448), (130, 640, 1408)])
+def test_ragged_shapes(gpu_lib, T, H, I):
+    x, w, _ = synth.custom_ffn(50 + T, T, H, I)
+    y = aflex.ffn_swiglu(x.to(DEV), w.to(DEV)).cpu()
+    check_rows(y, oracle.swiglu_ffn(x, w.w_gate, w.w_up, w.w_down), what=f"swiglu T={T} H={H} I={I}")
+
+
+@pytest.fixture(scope="module")
+def qwen3_weights():
+    w = synth.make_ffn_weights(2, 5120, 25600, device=DEV)
+    cpu64 = (w.w_gate.cpu().double(), w.w_up.cpu().double(), w.w_down.cpu().double())
+    yield w, cpu64
+    del w
+
+
+@pytest.mark.parametrize("T", [32, 128, 512])
+def test_qwen3_shape_sampled(gpu_lib, qwen3_weights, T):
+    w, (wg, wu, wd) = qwen3_weights
+    wl = synth.qwen3_swiglu(T, device=DEV, weights=w)
+    y = aflex.ffn_swiglu(wl.x, w).cpu()
+    rows = sample_rows(T, 6, seed=T, must=[0, T - 1])
+    ref = oracle.swiglu_ffn(wl.x[rows].cpu(), wg, wu, wd)
+    check_rows(y[rows], ref, what=f"qwen3 swiglu T={T} (sampled)")
+    y2 = aflex.ffn_swiglu(wl.x, w).cpu()
+    assert torch.equal(y, y2)

@@ -1,0 +1,77 @@
+"""HIP top-k MoE FFN vs the oracle: routing indices bit-exact, values within
+tolerance (through the C ABI)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2608_01891_amd import aflex, synth
+from tests.helpers import sample_rows
+from tests.parity import check_rows
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda:0"
+
+
+def _check_routing(r, logits, k, E):
+    ids, w = oracle.route_topk(logits.cpu(), k)
+    counts, offsets, sorted_ids, _ = oracle.routing_tables(ids, E)
+    assert torch.equal(r["topk_ids"].cpu().long(), ids)
+    assert torch.allclose(r["topk_w"].cpu().double(), w, rtol=2e-6, atol=1e-7)
+    assert torch.equal(r["expert_offsets"].cpu().long(), offsets)
+    assert torch.equal(r["sorted_pairs"].cpu().long(), sorted_ids)
+    return ids
+
+
+@pytest.mark.parametrize("T,H,I,E,k", [(37, 128, 192, 6, 3), (1, 64, 64, 8, 2), (100, 256, 320, 8, 2),
+                                       (9, 128, 128, 4, 4), (12, 128, 64, 1, 1), (300, 192, 256, 16, 8)])
+def test_small_shapes(gpu_lib, T, H, I, E, k):
+    x, w, logits = synth.custom_ffn(60 + T, T, H, I, E=E)
+    y, r = aflex.moe_ffn(x.to(DEV), w.to(DEV), logits.to(DEV), k, routing=True)
+    _check_routing(r, logits, k, E)
+    ref, _, _ = oracle.moe_ffn(x, logits, w.w_gate, w.w_up, w.w_down, k)
+    check_rows(y.cpu(), ref, what=f"moe T={T} E={E} k={k}")
+
+
+def test_skewed_routing_all_to_one_expert(gpu_lib):
+    T, H, I, E, k = 300, 128, 192, 8, 2
+    x, w, logits = synth.custom_ffn(70, T, H, I, E=E)
+    logits[:, 5] += 100.0  # every token picks expert 5 first: one segment of 300 rows
+    y, r = aflex.moe_ffn(x.to(DEV), w.to(DEV), logits.to(DEV), k, routing=True)
+    ids = _check_routing(r, logits, k, E)
+    assert (ids[:, 0] == 5).all()
+    ref, _, _ = oracle.moe_ffn(x, logits, w.w_gate, w.w_up, w.w_down, k)
+    check_rows(y.cpu(), ref, what="skewed moe")
+
+
+def test_ties_in_logits(gpu_lib):
+    T, H, I, E, k = 16, 64, 64, 4, 2
+    x, w, _ = synth.custom_ffn(71, T, H, I, E=E)
+    logits = torch.zeros(T, E)
+    logits[::2, 3] = 1.0
+    y, r = aflex.moe_ffn(x.to(DEV), w.to(DEV), logits.to(DEV), k, routing=True)
+    ids = _check_routing(r, logits, k, E)
+    assert ids[1].tolist() == [0, 1] and ids[0].tolist() == [3, 0]
+
+
+@pytest.fixture(scope="module")
+def mixtral():
+    wl = synth.mixtral_moe(device=DEV)
+    yield wl
+    del wl
+
+
+def test_mixtral_shape(gpu_lib, mixtral):
+    wl = mixtral
+    y, r = aflex.moe_ffn(wl.x, wl.ffn, wl.router_logits, 2, routing=True)
+    ids = _check_routing(r, wl.router_logits, 2, 8)
+    counts = torch.bincount(ids.reshape(-1), minlength=8)
+    assert counts.tolist() == [62, 61, 76, 65, 63, 67, 56, 62]
+    y = y.cpu()
+    toks = sample_rows(256, 6, seed=3, must=[0, 255])
+    f = wl.ffn
+    ref, _, _ = oracle.moe_ffn(wl.x.cpu(), wl.router_logits.cpu(), f.w_gate.cpu(), f.w_up.cpu(),
+                               f.w_down.cpu(), 2, token_indices=toks)
+    check_rows(y[toks], ref[toks], what="mixtral moe (sampled)")
+    y2 = aflex.moe_ffn(wl.x, wl.ffn, wl.router_logits, 2).cpu()
+    assert torch.equal(y, y2)

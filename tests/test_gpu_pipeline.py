@@ -1,0 +1,63 @@
+"""The two-stream interleaved A/F layer step vs the oracle (through the C ABI)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2608_01891_amd import aflex, synth
+from tests.helpers import sample_rows, sub_attention
+from tests.parity import check_rows
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda:0"
+
+
+def _small(E=4):
+    ctx = [5, 17, 40, 1, 33, 300, 9, 64]
+    a = synth.custom_attention(80, 8, 4, 2, 64, ctx, ctx_hi=320)
+    _, w, _ = synth.custom_ffn(80, 8, 256, 128, E=E)
+    logits = torch.from_numpy(np.random.default_rng(80).standard_normal((8, max(E, 1)),
+                                                                        dtype=np.float32))
+    return a, w, logits
+
+
+@pytest.mark.parametrize("mbs,L", [([8], 1), ([4, 4], 1), ([2, 2, 2, 2], 1), ([3, 5], 2),
+                                   ([1, 1, 6], 3)])
+def test_small_moe_pipeline(gpu_lib, mbs, L):
+    a, w, logits = _small()
+    y = aflex.af_pipeline_step(a.to(DEV), w.to(DEV), logits.to(DEV), 2, mbs, L=L).cpu()
+    ref = oracle.af_layer_steps(a, w, logits, 2, mbs, L=L)
+    check_rows(y, ref, what=f"pipeline mbs={mbs} L={L}")
+
+
+def test_small_dense_pipeline(gpu_lib):
+    a, w, _ = _small(E=0)
+    y = aflex.af_pipeline_step(a.to(DEV), w.to(DEV), None, 0, [5, 3], L=2).cpu()
+    check_rows(y, oracle.af_layer_steps(a, w, None, 0, [5, 3], L=2), what="dense pipeline")
+
+
+def test_repeated_calls_and_explicit_streams(gpu_lib):
+    a, w, logits = _small()
+    ad, wd, ld = a.to(DEV), w.to(DEV), logits.to(DEV)
+    sa, sf = torch.cuda.Stream(), torch.cuda.Stream()
+    cur = torch.cuda.current_stream()
+    sa.wait_stream(cur); sf.wait_stream(cur)
+    ys = [aflex.af_pipeline_step(ad, wd, ld, 2, [2, 6], stream_a=sa, stream_f=sf) for _ in range(3)]
+    cur.wait_stream(sf)
+    torch.cuda.synchronize()
+    assert torch.equal(ys[0], ys[1]) and torch.equal(ys[1], ys[2])
+
+
+def test_af_pipeline_workload_sampled(gpu_lib):
+    wl = synth.af_pipeline(device=DEV)
+    a, f = wl.attn, wl.ffn
+    y4 = aflex.af_pipeline_step(a, f, wl.router_logits, 2, wl.microbatches).cpu()
+    y1 = aflex.af_pipeline_step(a, f, wl.router_logits, 2, [256]).cpu()
+    rows = sample_rows(256, 6, seed=5, must=[0, 63, 64, 255])
+    sub = sub_attention(a, rows)
+    att = oracle.attention_decode(sub.q, sub.k_cache, sub.v_cache, sub.block_table, sub.context_lens)
+    ref, _, _ = oracle.moe_ffn(att.reshape(len(rows), -1), wl.router_logits.cpu()[rows],
+                               f.w_gate.cpu(), f.w_up.cpu(), f.w_down.cpu(), 2)
+    check_rows(y4[rows], ref, what="A/F pipeline M=4 (sampled)")
+    check_rows(y1[rows], ref, what="A/F pipeline M=1 (sampled)")
+    check_rows(y4, y1.double(), what="M=4 vs M=1 over all rows")
