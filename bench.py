@@ -1,0 +1,386 @@
+#!/usr/bin/env python3
+"""Benchmark of the decode-step A/F operators on one MI355X.
+
+A step is one interleaved A/F layer step of the Mixtral-shaped pipeline
+workload (B = 256 decode tokens, 32/8 heads, D = 128, paged bf16 KV with
+lognormal contexts of median 4096; top-2 of 8 SwiGLU experts, H = 4096,
+I = 14336; M = 4 microbatches on two HIP streams): every microbatch's paged
+GQA attention and its MoE FFN. The JSON line reports tokens/s of that step,
+the roofline of its dominant kernel (the grouped gate/up GEMM, HBM-bound),
+the oracle's CPU rate on a bounded sample, and per-operator throughput on the
+other workloads (Qwen3-32B attention and dense SwiGLU, Mixtral MoE).
+
+    python bench.py [--steps K] [--warmup W] [--gpus 1]
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_HBM = 8.0e12      # B/s, MI355X HBM3E
+PEAK_BF16 = 2.5e15     # flop/s, dense bf16 MFMA
+METRIC = "attn-decode HBM GB/s & FFN bf16 TFLOPS vs peak; A/F layer-step tokens/s"
+DOMINANT = "gemm_gate_up"
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gemm_gate_up_af_pipeline_traffic.json")
+KERNEL_SOURCES = ["gemm.h", "gemm_dispatch.hip", "ffn_plan.h", "moe.hip"]
+
+
+def kernel_hash():
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, "paper_2608_01891_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def parse():
+    p = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=20)
+    p.add_argument("--warmup", type=int, default=5)
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--no-operators", action="store_true", help="skip the per-operator section")
+    p.add_argument("--counters-pass", action="store_true",
+                   help="only warm-up + steps of the layer step and a 1 GiB copy (for rocprofv3 --pmc)")
+    return p.parse_args()
+
+
+def timed(fn, reps, stream=None):
+    """Average ms of fn() over reps, HIP events on the current stream."""
+    import torch
+    s = stream or torch.cuda.current_stream()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(s)
+    for _ in range(reps):
+        fn()
+    e1.record(s)
+    e1.synchronize()
+    return e0.elapsed_time(e1) / reps
+
+
+def energy_reader():
+    """Callable returning the GPU's accumulated energy in joules, or None."""
+    try:
+        import amdsmi
+        amdsmi.amdsmi_init()
+        h = amdsmi.amdsmi_get_processor_handles()[0]
+
+        def read():
+            e = amdsmi.amdsmi_get_energy_count(h)
+            acc = e.get("energy_accumulator", e.get("power"))
+            return float(acc) * float(e["counter_resolution"]) * 1e-6
+        read()
+        return read
+    except Exception:
+        return None
+
+
+def topk_ids_host(logits, k):
+    import numpy as np
+    return np.argsort(-logits, axis=1, kind="stable")[:, :k]
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU only: the decode-step operators are built and timed on a "
+              "single MI355X (run with --gpus 1).", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2608_01891_amd import aflex, plan, synth
+
+    aflex.load()  # fails loudly if the HIP library is not built
+    if not torch.cuda.is_available():
+        raise SystemExit("bench.py needs a GPU")
+    dev = "cuda:0"
+    torch.cuda.set_device(0)
+
+    # ---------------- the headline step: interleaved A/F layer step ----------------
+    wl = synth.af_pipeline(device=dev)
+    a, f, logits = wl.attn, wl.ffn, wl.router_logits
+    mbs = wl.microbatches
+    B, H, I, k = a.B, f.H, f.I, wl.top_k
+    y = torch.empty(B, H, dtype=torch.bfloat16, device=dev)
+    sa, sf = aflex.pipeline_streams(dev)
+    pws = aflex.Workspace()
+
+    def step(m=mbs):
+        aflex.af_pipeline_step(a, f, logits, k, m, y=y, stream_a=sa, stream_f=sf, ws=pws, join=False)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    if args.counters_pass:
+        for _ in range(args.steps):
+            step()
+        src = torch.empty(1 << 29, dtype=torch.int16, device=dev)  # 1 GiB
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"counters_pass": True, "steps": args.steps, "copy_bytes": 2 * src.numel()}))
+        return
+
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    ms_step = (t1 - t0) * 1e3 / args.steps
+
+    # same steps again with HIP events around the dominant kernel on its stream
+    aflex.profile_start([DOMINANT, "attn_split", "gemm_down"])
+    t2 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    t3 = time.perf_counter()
+    prof = aflex.profile_stop()
+    ms_step_ev = (t3 - t2) * 1e3 / args.steps
+
+    lg = logits.cpu().numpy()
+    ctx = a.context_lens.cpu().numpy().astype(np.int64)
+    kv_bytes_total = int(ctx.sum()) * a.Hkv * a.D * 2 * 2
+    w_bytes_expert = 3 * I * H * 2
+    # algorithmic bytes of the gate/up GEMM per launch: touched experts' W_g and
+    # W_u, the microbatch's x rows, and the bf16 h rows it writes
+    gate_bytes, gate_flops, step_bytes = [], [], kv_bytes_total
+    off = 0
+    for n in mbs:
+        ids = topk_ids_host(lg[off:off + n], k)
+        touched = len(np.unique(ids))
+        gate_bytes.append(touched * 2 * I * H * 2 + n * H * 2 + n * k * I * 2)
+        gate_flops.append(n * k * 2 * 2 * H * I)
+        step_bytes += touched * w_bytes_expert + n * H * 2 * 2
+        off += n
+    n_launch, tot_ms, mn_ms, mx_ms = prof[DOMINANT]
+    avg_ms = tot_ms / n_launch
+    gate_avg_bytes = sum(gate_bytes) / len(gate_bytes)
+    achieved = gate_avg_bytes / (avg_ms * 1e-3)
+
+    traffic = None
+    if os.path.exists(TRAFFIC_FILE):
+        with open(TRAFFIC_FILE) as fh:
+            tf = json.load(fh)
+        if tf.get("kernel_hash") == kernel_hash():
+            traffic = tf.get("bytes_per_launch")
+
+    result = {
+        "metric": METRIC,
+        "value": round(B / (ms_step * 1e-3), 1),
+        "unit": "tok/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": "af-pipeline: Mixtral-8x7B-shaped decode layer step, B=256, "
+                               "32/8 heads x 128, paged bf16 KV (block 16, lognormal ctx median 4096, "
+                               "sum 1392790 tokens), top-2 of 8 SwiGLU experts H=4096 I=14336, "
+                               "M=4 microbatches of 64 on 2 HIP streams, L=1",
+                   "global_batch": B, "microbatches": mbs, "kv_bytes": kv_bytes_total,
+                   "step_algorithmic_bytes": step_bytes,
+                   "step_hbm_fraction": round(step_bytes / (ms_step * 1e-3) / PEAK_HBM, 4)},
+        "roofline": {"kernel": DOMINANT, "bound": "hbm", "achieved": round(achieved / 1e9, 1),
+                     "peak": PEAK_HBM / 1e9, "unit": "GB/s", "frac": round(achieved / PEAK_HBM, 4),
+                     "traffic": traffic, "bytes_per_launch": int(gate_avg_bytes),
+                     "avg_launch_ms": round(avg_ms, 5), "launches": n_launch,
+                     "min_launch_ms": round(mn_ms, 5), "max_launch_ms": round(mx_ms, 5),
+                     "ms_per_step_with_events": round(ms_step_ev, 4),
+                     "kernel_hash": kernel_hash()},
+    }
+    result["kernels_in_step"] = {kname: {"launches": v[0], "avg_ms": round(v[1] / v[0], 5)}
+                                 for kname, v in prof.items()}
+
+    # ---------------- energy per token (where the counter is readable) -------------
+    read_energy = energy_reader()
+    if read_energy is not None:
+        n = max(1, int(1.5 / (ms_step * 1e-3)))
+        torch.cuda.synchronize()
+        e0, t0 = read_energy(), time.perf_counter()
+        for _ in range(n):
+            step()
+        torch.cuda.synchronize()
+        e1, t1 = read_energy(), time.perf_counter()
+        result["energy"] = {"joules_per_token": round((e1 - e0) / (n * B), 6),
+                            "avg_watts": round((e1 - e0) / (t1 - t0), 1), "steps": n}
+    else:
+        result["energy"] = "n/a (energy counter not readable)"
+
+    # ---------------- pipeline variants and Eq. 2 comparison -------------------------
+    if not args.no_operators:
+        ops = {}
+        variants = {}
+        for M in (1, 2, 4):
+            m = plan.equal_microbatches(B, M)
+            step(m)
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            for _ in range(args.steps):
+                step(m)
+            torch.cuda.synchronize()
+            ms = (time.perf_counter() - t0) * 1e3 / args.steps
+            variants[f"M={M}"] = {"ms": round(ms, 4), "tok_per_s": round(B / (ms * 1e-3), 1)}
+        # standalone stage times per microbatch (one stream, no overlap)
+        t_a = t_f = 0.0
+        off = 0
+        x_mb = torch.empty(64, H, dtype=torch.bfloat16, device=dev)
+        for n in mbs:
+            am = synth.AttnInputs(q=a.q[off:off + n], k_cache=a.k_cache, v_cache=a.v_cache,
+                                  block_table=a.block_table[off:off + n],
+                                  context_lens=a.context_lens[off:off + n], B=n, Hq=a.Hq, Hkv=a.Hkv,
+                                  D=a.D, block_size=16, max_blocks=a.max_blocks,
+                                  num_blocks=a.num_blocks, max_context_len=a.max_context_len)
+            out = torch.empty(n, a.Hq, a.D, dtype=torch.bfloat16, device=dev)
+            aflex.attn_decode(am, out=out)
+            t_a += timed(lambda: aflex.attn_decode(am, out=out), 5)
+            xm = out.view(n, H)
+            lm = logits[off:off + n]
+            aflex.moe_ffn(xm, f, lm, k, y=x_mb[:n])
+            t_f += timed(lambda: aflex.moe_ffn(xm, f, lm, k, y=x_mb[:n]), 5)
+            off += n
+        variants["standalone_sum_ms"] = {"attention": round(t_a, 4), "ffn": round(t_f, 4),
+                                         "serial": round(t_a + t_f, 4)}
+        variants["eq2_ms"] = {"M=1": round(plan.eq2_layer_time(t_a, t_f, 0.0, 1), 4),
+                              "M=4": round(plan.eq2_layer_time(t_a, t_f, 0.0, 4), 4)}
+        variants["byte_roofline_ms"] = round(step_bytes / PEAK_HBM * 1e3, 4)
+        variants["t_F_over_t_A"] = round(t_f / t_a, 3)
+        ops["af_pipeline"] = variants
+
+        # Qwen3-32B decode attention, 3 KV-pool copies rotated so the 256 MB MALL cannot hold them
+        wq = synth.qwen3_attention(device=dev).attn
+        copies = [wq] + [synth.AttnInputs(**{**wq.__dict__, "k_cache": wq.k_cache.clone(),
+                                            "v_cache": wq.v_cache.clone()}) for _ in range(2)]
+        outq = torch.empty(wq.B, wq.Hq, wq.D, dtype=torch.bfloat16, device=dev)
+        cq = wq.context_lens.cpu().numpy().astype(np.int64)
+        abytes = (int(cq.sum()) * wq.Hkv * wq.D * 2 * 2 + 2 * wq.B * wq.Hq * wq.D * 2
+                  + int(((cq + 15) // 16).sum()) * 4 + wq.B * 4)
+        aflops = 4 * int(cq.sum()) * wq.Hq * wq.D
+        it = [0]
+
+        def run_attn():
+            aflex.attn_decode(copies[it[0] % 3], out=outq)
+            it[0] += 1
+        for _ in range(3):
+            run_attn()
+        aflex.profile_start(["attn_split", "attn_merge"])
+        ms = timed(run_attn, 30)
+        kp = aflex.profile_stop()
+        ops["attention_qwen3_B64"] = {
+            "ms": round(ms, 5), "GB_per_s": round(abytes / (ms * 1e-3) / 1e9, 1),
+            "hbm_frac": round(abytes / (ms * 1e-3) / PEAK_HBM, 4), "bytes": abytes,
+            "tflops": round(aflops / (ms * 1e-3) / 1e12, 2), "tok_per_s": round(wq.B / (ms * 1e-3), 1),
+            "kernels": {kname: round(v[1] / v[0], 5) for kname, v in kp.items()}}
+        del copies, wq
+
+        # Full-batch long-context attention of the pipeline workload
+        outl = torch.empty(B, a.Hq, a.D, dtype=torch.bfloat16, device=dev)
+        aflex.attn_decode(a, out=outl)
+        ms = timed(lambda: aflex.attn_decode(a, out=outl), 10)
+        lbytes = kv_bytes_total + 2 * B * a.Hq * a.D * 2
+        ops["attention_longctx_B256"] = {"ms": round(ms, 5),
+                                         "GB_per_s": round(lbytes / (ms * 1e-3) / 1e9, 1),
+                                         "hbm_frac": round(lbytes / (ms * 1e-3) / PEAK_HBM, 4)}
+
+        # Qwen3-32B dense SwiGLU, T in {32, 128, 256, 512}
+        wd = synth.make_ffn_weights(2, 5120, 25600, device=dev)
+        for T in (32, 128, 256, 512):
+            wlT = synth.qwen3_swiglu(T, device=dev, weights=wd)
+            yT = torch.empty(T, 5120, dtype=torch.bfloat16, device=dev)
+            aflex.ffn_swiglu(wlT.x, wd, y=yT)
+            aflex.profile_start(["gemm_gate_up", "gemm_down", "splitk_reduce"])
+            ms = timed(lambda: aflex.ffn_swiglu(wlT.x, wd, y=yT), 10)
+            kp = aflex.profile_stop()
+            flops = 6 * T * 5120 * 25600
+            byts = 3 * 5120 * 25600 * 2 + 2 * T * 5120 * 2
+            att = min(PEAK_BF16, flops / byts * PEAK_HBM)
+            ops[f"swiglu_qwen3_T{T}"] = {
+                "ms": round(ms, 5), "tflops": round(flops / (ms * 1e-3) / 1e12, 1),
+                "mfma_frac": round(flops / (ms * 1e-3) / PEAK_BF16, 4),
+                "attainable_frac": round(flops / (ms * 1e-3) / att, 4),
+                "GB_per_s": round(byts / (ms * 1e-3) / 1e9, 1),
+                "hbm_frac": round(byts / (ms * 1e-3) / PEAK_HBM, 4),
+                "tok_per_s": round(T / (ms * 1e-3), 1),
+                "kernels": {kname: round(v[1] / v[0], 5) for kname, v in kp.items()}}
+        del wd
+
+        # Mixtral MoE, T = 256 (and T = 2048 supplementary)
+        for T, seed in ((256, 3), (2048, 103)):
+            wm = synth.mixtral_moe(device=dev, T=T, seed=seed, weights=f if T == 2048 else None)
+            yT = torch.empty(T, H, dtype=torch.bfloat16, device=dev)
+            aflex.moe_ffn(wm.x, wm.ffn, wm.router_logits, 2, y=yT)
+            aflex.profile_start(None)
+            ms = timed(lambda: aflex.moe_ffn(wm.x, wm.ffn, wm.router_logits, 2, y=yT), 10)
+            kp = aflex.profile_stop()
+            ids = topk_ids_host(wm.router_logits.cpu().numpy(), 2)
+            touched = len(np.unique(ids))
+            flops = T * 2 * 6 * H * I
+            byts = touched * w_bytes_expert + 2 * T * H * 2
+            att = min(PEAK_BF16, flops / byts * PEAK_HBM)
+            ops[f"moe_mixtral_T{T}"] = {
+                "ms": round(ms, 5), "tflops": round(flops / (ms * 1e-3) / 1e12, 1),
+                "mfma_frac": round(flops / (ms * 1e-3) / PEAK_BF16, 4),
+                "attainable_frac": round(flops / (ms * 1e-3) / att, 4),
+                "GB_per_s": round(byts / (ms * 1e-3) / 1e9, 1),
+                "hbm_frac": round(byts / (ms * 1e-3) / PEAK_HBM, 4),
+                "tok_per_s": round(T / (ms * 1e-3), 1),
+                "kernels": {kname: round(v[1] / v[0], 5) for kname, v in kp.items()}}
+            del wm
+        result["operators"] = ops
+
+    # ---------------- CPU baseline: the oracle on a bounded sample -------------------
+    if not args.no_cpu_baseline:
+        import oracle
+
+        def oracle_sample(n_seq):
+            bt = a.block_table[:n_seq].cpu()
+            cl = a.context_lens[:n_seq].cpu()
+            phys, table = [], torch.full((n_seq, a.max_blocks), -1, dtype=torch.int32)
+            for i in range(n_seq):
+                nb = -(-int(cl[i]) // 16)
+                table[i, :nb] = torch.arange(len(phys), len(phys) + nb, dtype=torch.int32)
+                phys += bt[i, :nb].tolist()
+            idx = torch.tensor(phys, device=dev)
+            sub = synth.AttnInputs(q=a.q[:n_seq].cpu(), k_cache=a.k_cache[idx].cpu(),
+                                   v_cache=a.v_cache[idx].cpu(), block_table=table, context_lens=cl,
+                                   B=n_seq, Hq=a.Hq, Hkv=a.Hkv, D=a.D, block_size=16,
+                                   max_blocks=a.max_blocks, num_blocks=len(phys),
+                                   max_context_len=a.max_context_len)
+            wts = synth.FFNWeights(f.w_gate.cpu(), f.w_up.cpu(), f.w_down.cpu(), H, I, f.E)
+            lgs = logits[:n_seq].cpu()
+            t0 = time.perf_counter()
+            oracle.af_layer_steps(sub, wts, lgs, k, [n_seq], L=1)
+            return time.perf_counter() - t0, int(cl.sum())
+
+        n_seq = 8
+        dt, ntok = oracle_sample(n_seq)
+        if dt < 5.0:  # grow the sample towards ~15 s of oracle work
+            n_seq = min(B, max(n_seq, int(n_seq * 15.0 / max(dt, 1e-3))))
+            dt, ntok = oracle_sample(n_seq)
+        result["cpu_baseline"] = {
+            "value": round(n_seq / dt, 4), "unit": "tok/s", "cores": torch.get_num_threads(),
+            "kind": "oracle",
+            "sample": f"first {n_seq} of the 256 sequences of the pipeline workload ({ntok} cached "
+                      f"tokens): their attention and top-2 MoE FFN in the float64 oracle, {dt:.1f} s"}
+
+    print(json.dumps(result))
+
+
+if __name__ == "__main__":
+    main()

@@ -143,6 +143,22 @@ aflex_status aflex_af_pipeline_step(const aflex_attn_args *attn, const aflex_ffn
                                     void *workspace, size_t workspace_bytes,
                                     aflex_stream stream_a, aflex_stream stream_f);
 
+/* ------------------------------------------------------------------------ */
+/* Per-kernel timing, the single-GPU analogue of the paper's per-operator     */
+/* latency profiling (section 4.1; section 5, "Profiling module"). Between    */
+/* aflex_profile_start and aflex_profile_stop, every library kernel whose     */
+/* name is in the comma-separated list `kernels` (NULL or "" = all) is        */
+/* bracketed by two HIP events on the stream it is launched on. Kernel names: */
+/* attn_split, attn_merge, gemm_gate_up, gemm_down, splitk_reduce, moe_route, */
+/* moe_combine. aflex_profile_stop waits for those events and writes one line */
+/* per kernel into `report` (host buffer of `len` bytes, truncated to fit):   */
+/*   "<name> <launches> <total_ms> <min_ms> <max_ms>
+"                      */
+/* Off by default; while off no event is recorded.                            */
+/* ------------------------------------------------------------------------ */
+aflex_status aflex_profile_start(const char *kernels);
+aflex_status aflex_profile_stop(char *report, size_t len);
+
 /* Thread-local message describing the last non-OK status of this thread. */
 const char *aflex_last_error(void);
 /* Library version string. */

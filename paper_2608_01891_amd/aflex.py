@@ -79,10 +79,32 @@ def load():
         fn = getattr(lib, name)
         fn.argtypes = args
         fn.restype = ctypes.c_int
+    lib.aflex_profile_start.argtypes = [ctypes.c_char_p]
+    lib.aflex_profile_start.restype = ctypes.c_int
+    lib.aflex_profile_stop.argtypes = [ctypes.c_char_p, ctypes.c_size_t]
+    lib.aflex_profile_stop.restype = ctypes.c_int
     lib.aflex_last_error.restype = ctypes.c_char_p
     lib.aflex_version.restype = ctypes.c_char_p
     _lib = lib
     return lib
+
+
+def profile_start(kernels=None):
+    """Start per-kernel event timing for the named library kernels (None = all)."""
+    lib = load()
+    _check(lib.aflex_profile_start(",".join(kernels).encode() if kernels else None))
+
+
+def profile_stop():
+    """Stop timing; {kernel: (launches, total_ms, min_ms, max_ms)}."""
+    lib = load()
+    buf = ctypes.create_string_buffer(1 << 16)
+    _check(lib.aflex_profile_stop(buf, len(buf)))
+    out = {}
+    for line in buf.value.decode().splitlines():
+        name, n, tot, mn, mx = line.split()
+        out[name] = (int(n), float(tot), float(mn), float(mx))
+    return out
 
 
 def _check(status: int):

@@ -30,6 +30,7 @@
 
 #include "common.h"
 #include "kernels.h"
+#include "profile.h"
 
 namespace aflex {
 
@@ -299,12 +300,20 @@ hipError_t launch_attn_decode(const aflex_attn_args& a, void* ws, hipStream_t st
   p.part_ml = reinterpret_cast<float*>(static_cast<char*>(ws) +
                                        align_up(rows * a.D * sizeof(float), 256));
   dim3 grid(a.B * a.Hkv, p.max_splits);
-  if (a.D == 128) {
-    attn_split_kernel<128><<<grid, 256, 0, stream>>>(p);
-    if (p.max_splits > 1) attn_merge_kernel<128><<<(a.B * a.Hq + kWaves - 1) / kWaves, 256, 0, stream>>>(p);
-  } else {
-    attn_split_kernel<64><<<grid, 256, 0, stream>>>(p);
-    if (p.max_splits > 1) attn_merge_kernel<64><<<(a.B * a.Hq + kWaves - 1) / kWaves, 256, 0, stream>>>(p);
+  const unsigned merge_grid = (a.B * a.Hq + kWaves - 1) / kWaves;
+  {
+    ProfScope ps("attn_split", stream);
+    if (a.D == 128)
+      attn_split_kernel<128><<<grid, 256, 0, stream>>>(p);
+    else
+      attn_split_kernel<64><<<grid, 256, 0, stream>>>(p);
+  }
+  if (p.max_splits > 1) {
+    ProfScope ps("attn_merge", stream);
+    if (a.D == 128)
+      attn_merge_kernel<128><<<merge_grid, 256, 0, stream>>>(p);
+    else
+      attn_merge_kernel<64><<<merge_grid, 256, 0, stream>>>(p);
   }
   return hipGetLastError();
 }

@@ -12,6 +12,7 @@
 #include "ffn_plan.h"
 #include "gemm.h"
 #include "kernels.h"
+#include "profile.h"
 
 namespace aflex {
 
@@ -82,6 +83,7 @@ hipError_t launch_swiglu(const aflex_ffn_args& f, void* ws, hipStream_t stream) 
   e = launch_down(pl.bm, pl.down_splits > 1, d, stream);
   if (e != hipSuccess || pl.down_splits == 1) return e;
   const long long n4 = (long long)f.T * f.H / 4;
+  ProfScope ps("splitk_reduce", stream);
   splitk_reduce_kernel<<<(unsigned)((n4 + 255) / 256), 256, 0, stream>>>(P, d.p_split_stride, pl.down_splits, n4,
                                                                        f.y);
   return hipGetLastError();

@@ -18,6 +18,7 @@
 #include "ffn_plan.h"
 #include "gemm.h"
 #include "kernels.h"
+#include "profile.h"
 
 namespace aflex {
 
@@ -207,9 +208,12 @@ hipError_t launch_moe(const aflex_ffn_args& f, void* ws, hipStream_t stream) {
   uint16_t* h = reinterpret_cast<uint16_t*>(w + L.h);
   float* P = reinterpret_cast<float*>(w + L.P);
 
-  moe_route_kernel<<<1, 256, 0, stream>>>(f.router_logits, f.T, f.E, f.k, L.bm, ids, wts, offsets, sorted, pos,
-                                          tile_map, num_tiles, f.topk_ids, f.topk_w, f.expert_offsets,
-                                          f.sorted_pairs);
+  {
+    ProfScope ps("moe_route", stream);
+    moe_route_kernel<<<1, 256, 0, stream>>>(f.router_logits, f.T, f.E, f.k, L.bm, ids, wts, offsets, sorted, pos,
+                                            tile_map, num_tiles, f.topk_ids, f.topk_w, f.expert_offsets,
+                                            f.sorted_pairs);
+  }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
 
@@ -259,6 +263,7 @@ hipError_t launch_moe(const aflex_ffn_args& f, void* ws, hipStream_t stream) {
   if (e != hipSuccess) return e;
 
   dim3 grid(f.T, (f.H / 4 + 255) / 256);
+  ProfScope ps("moe_combine", stream);
   moe_combine_kernel<<<grid, 256, 0, stream>>>(P, d.p_split_stride, L.down_splits, pos, wts, f.k, f.H, f.y);
   return hipGetLastError();
 }
