@@ -96,7 +96,7 @@ aflex_status hip_status(hipError_t e, const char* who) {
 // ---------------------------------------------------------------------------
 // Pipeline driver.
 struct PipeLayout {
-  size_t attn_out, attn_ws, ffn_ws, total;
+  size_t attn_out, attn_ws, route_ws, route_stride, ffn_ws, total;
 };
 
 aflex_attn_args mb_attn(const aflex_attn_args& a, int off, int n) {
@@ -124,20 +124,24 @@ aflex_ffn_args mb_ffn(const aflex_ffn_args& f, int off, int n) {
 
 PipeLayout pipe_layout(const aflex_attn_args& a, const aflex_ffn_args& f, int M, const int32_t* mb) {
   PipeLayout L;
-  size_t aw = 0, fw = 0;
+  size_t aw = 0, fw = 0, rw = 0;
   int off = 0;
   for (int i = 0; i < M; ++i) {
     aflex_attn_args am = mb_attn(a, off, mb[i]);
     aflex_ffn_args fm = mb_ffn(f, off, mb[i]);
     size_t x = aflex::attn_workspace_bytes(am);
-    size_t y = f.E ? aflex::moe_workspace_bytes(fm) : aflex::swiglu_workspace_bytes(fm);
+    size_t y = f.E ? aflex::moe_expert_bytes(fm) : aflex::swiglu_workspace_bytes(fm);
+    size_t z = f.E ? aflex::moe_route_bytes(fm) : 0;
     aw = x > aw ? x : aw;
     fw = y > fw ? y : fw;
+    rw = z > rw ? z : rw;
     off += mb[i];
   }
   L.attn_out = 0;
   L.attn_ws = aflex::align_up((size_t)a.B * a.Hq * a.D * 2, 256);
-  L.ffn_ws = L.attn_ws + aflex::align_up(aw, 256);
+  L.route_ws = L.attn_ws + aflex::align_up(aw, 256);
+  L.route_stride = aflex::align_up(rw, 256);
+  L.ffn_ws = L.route_ws + (size_t)M * L.route_stride;
   L.total = L.ffn_ws + aflex::align_up(fw, 256);
   return L;
 }
@@ -270,6 +274,18 @@ aflex_status aflex_af_pipeline_step(const aflex_attn_args* a, const aflex_ffn_ar
   if ((e = hipEventRecord(entry, sf)) != hipSuccess) return hip_status(e, "pipeline");
   if ((e = hipStreamWaitEvent(sa, entry, 0)) != hipSuccess) return hip_status(e, "pipeline");
 
+  // Routing depends only on the router logits: do it for every microbatch up
+  // front on stream_f, where it overlaps the first attention.
+  if (f->E) {
+    int off = 0;
+    for (int i = 0; i < M; ++i) {
+      aflex_ffn_args fm = mb_ffn(*f, off, mb[i]);
+      if ((e = aflex::launch_moe_route(fm, w + P.route_ws + (size_t)i * P.route_stride, sf)) != hipSuccess)
+        return hip_status(e, "pipeline: route");
+      off += mb[i];
+    }
+  }
+
   for (int l = 0; l < L; ++l) {
     int off = 0;
     for (int i = 0; i < M; ++i) {
@@ -283,7 +299,8 @@ aflex_status aflex_af_pipeline_step(const aflex_attn_args* a, const aflex_ffn_ar
       if ((e = hipStreamWaitEvent(sf, evA[i], 0)) != hipSuccess) return hip_status(e, "pipeline");
       aflex_ffn_args fm = mb_ffn(*f, off, n);
       fm.x = attn_out + (size_t)off * H;
-      e = f->E ? aflex::launch_moe(fm, ffn_ws, sf) : aflex::launch_swiglu(fm, ffn_ws, sf);
+      e = f->E ? aflex::launch_moe_experts(fm, w + P.route_ws + (size_t)i * P.route_stride, ffn_ws, sf)
+               : aflex::launch_swiglu(fm, ffn_ws, sf);
       if (e != hipSuccess) return hip_status(e, "pipeline: ffn");
       if ((e = hipEventRecord(evF[i], sf)) != hipSuccess) return hip_status(e, "pipeline");
       off += n;

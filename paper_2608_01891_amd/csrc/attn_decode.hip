@@ -232,8 +232,26 @@ __global__ __launch_bounds__(256, 2) void attn_split_kernel(AttnParams p) {
   }
 }
 
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
+  return v;
+}
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+
+// One wave per (sequence, head). Lanes first reduce the split maxima and
+// denominators in parallel, then each lane sums 4 consecutive d of every
+// NG-th split (NG = 64 / (D/4) lane groups) with 16-byte loads, and the groups
+// are combined with xor shuffles; the summation order is fixed.
 template <int D>
 __global__ __launch_bounds__(256) void attn_merge_kernel(AttnParams p) {
+  constexpr int D4 = D / 4;
+  constexpr int NG = 64 / D4;
   const int wave = threadIdx.x >> 6;
   const int lane = threadIdx.x & 63;
   const int row = blockIdx.x * kWaves + wave;  // (b, h)
@@ -244,16 +262,30 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnParams p) {
   if (nsplit <= 1) return;  // written by the split kernel
   const float* ml = p.part_ml + (size_t)row * p.max_splits * 2;
   float M = kNegInf;
-  for (int s = 0; s < nsplit; ++s) M = fmaxf(M, ml[2 * s]);
+  for (int s = lane; s < nsplit; s += 64) M = fmaxf(M, ml[2 * s]);
+  M = wave_max(M);
   const float Mu = (M == kNegInf) ? 0.f : M;
   float L = 0.f;
-  for (int s = 0; s < nsplit; ++s) L += fast_exp2(ml[2 * s] - Mu) * ml[2 * s + 1];
+  for (int s = lane; s < nsplit; s += 64) L += fast_exp2(ml[2 * s] - Mu) * ml[2 * s + 1];
+  L = wave_sum(L);
   const float inv = L > 0.f ? 1.f / L : 0.f;
-  const float* po = p.part_o + (size_t)row * p.max_splits * D;
-  for (int d = lane; d < D; d += 64) {
-    float O = 0.f;
-    for (int s = 0; s < nsplit; ++s) O += fast_exp2(ml[2 * s] - Mu) * po[(size_t)s * D + d];
-    p.out[(size_t)row * D + d] = f2bf(O * inv);
+  const int grp = lane / D4, d4 = lane - grp * D4;
+  const float* po = p.part_o + (size_t)row * p.max_splits * D + d4 * 4;
+  f32x4 O = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll 4
+  for (int s = grp; s < nsplit; s += NG) O += fast_exp2(ml[2 * s] - Mu) * *reinterpret_cast<const f32x4*>(po + (size_t)s * D);
+#pragma unroll
+  for (int o = D4; o < 64; o <<= 1) {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) O[e] += __shfl_xor(O[e], o);
+  }
+  if (grp == 0) {
+    ushort4 v;
+    v.x = f2bf(O[0] * inv);
+    v.y = f2bf(O[1] * inv);
+    v.z = f2bf(O[2] * inv);
+    v.w = f2bf(O[3] * inv);
+    *reinterpret_cast<ushort4*>(p.out + (size_t)row * D + d4 * 4) = v;
   }
 }
 

@@ -73,7 +73,7 @@ hipError_t launch_swiglu(const aflex_ffn_args& f, void* ws, hipStream_t stream) 
   d.splits = pl.down_splits;
   d.M = f.T;
   d.max_mtiles = (f.T + pl.bm - 1) / pl.bm;
-  d.n_ntiles = (f.H + kDownBN - 1) / kDownBN;
+  d.n_ntiles = (f.H + down_bn(pl.bm) - 1) / down_bn(pl.bm);
   d.mt_major = 0;
   d.C = f.y;
   d.ldc = f.H;

@@ -6,8 +6,10 @@
 
 namespace aflex {
 
-constexpr int kGateBN = 64;   // output columns per gate/up tile (x2 weight rows)
+constexpr int kGateBN = 64;  // output columns per gate/up tile (x2 weight rows)
+
 constexpr int kDownBN = 128;  // output columns per down tile
+inline int down_bn(int) { return kDownBN; }
 
 struct FfnPlan {
   int bm;           // rows per m-tile: 32, 64 or 128
@@ -39,7 +41,7 @@ inline FfnPlan plan_dense(int T, int H, int I) {
   FfnPlan pl;
   pl.bm = T <= 32 ? 32 : (T <= 64 ? 64 : 128);
   const int mtiles = (T + pl.bm - 1) / pl.bm;
-  const int ntiles = (H + kDownBN - 1) / kDownBN;
+  const int ntiles = (H + down_bn(pl.bm) - 1) / down_bn(pl.bm);
   plan_splits(mtiles * ntiles, I, 512, 8, &pl.down_splits, &pl.down_kps);
   return pl;
 }

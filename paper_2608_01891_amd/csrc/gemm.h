@@ -4,9 +4,12 @@
 // is how the MoE reads its token-permuted input without materialising it),
 // B [N, K] holds weights in the [out_features, in_features] layout, so both
 // operands have the contraction index contiguous and every MFMA operand is
-// one 16-byte LDS read. Tiles of BM x BN x 64 are staged global -> registers
-// -> LDS with a double buffer (the next k-step's loads are in flight while
-// the current one is multiplied) using v_mfma_f32_16x16x32_bf16.
+// one 16-byte LDS read. Tiles of BM x BN x 64 stream from HBM straight into a
+// ring of 3-4 LDS stages (global_load_lds_dwordx4, no register staging), so
+// the loads of the next k-steps are in flight while kt is multiplied
+// (v_mfma_f32_16x16x32_bf16). At decode batch sizes these GEMMs stream
+// weights, so the depth of the load pipeline, not the MFMA rate, sets their
+// speed.
 //
 // Variants (template flags):
 //   DUAL    two weight matrices (gate, up) share the A tile; the epilogue
@@ -52,25 +55,47 @@ struct GemmParams {
   int ldp;
 };
 
+// 32-bit LDS offset of a pointer into a __shared__ array.
+__device__ __forceinline__ uint32_t lds_offset(const void* p) {
+  return static_cast<uint32_t>(reinterpret_cast<size_t>((__attribute__((address_space(3))) const void*)p));
+}
+
+// Direct HBM -> LDS load of 16 bytes per lane: lane l writes LDS bytes
+// [lds + 16 l, lds + 16 l + 16). Issued as inline assembly so the compiler's
+// wait-count pass does not serialise it against reads of other LDS stages;
+// callers order it with explicit s_waitcnt vmcnt and barriers.
+__device__ __forceinline__ void lds_dma16(const void* gptr, uint32_t lds) {
+  const uint32_t lds_s = __builtin_amdgcn_readfirstlane(lds);  // uniform across the wave
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(gptr), "s"(lds_s) : "memory", "m0");
+}
+
 __device__ __forceinline__ int xcd_remap(int w, int nwg) {
   const int q = nwg >> 3, rem = nwg & 7, x = w & 7, j = w >> 3;
   return (x < rem ? x * (q + 1) : rem * (q + 1) + (x - rem) * q) + j;
 }
 
 template <int BM, int BN, int WM, int WN, bool DUAL, bool OUT_F32>
-__global__ __launch_bounds__(256, 2) void gemm_nt_kernel(GemmParams p) {
-  constexpr int BK = 64;
-  constexpr int LDK = BK + 8;  // padded LDS row (144 B): conflict-free 16-byte fragment reads
+__global__ __launch_bounds__(256, BM >= 128 ? 1 : 2) void gemm_nt_kernel(GemmParams p) {
+  constexpr int BK = 64;  // one LDS row = 64 bf16 = 128 B = 8 chunks of 16 B
   constexpr int NB = DUAL ? 2 : 1;
   constexpr int WTM = BM / WM, WTN = BN / WN;
   constexpr int TM = WTM / 16, TN = WTN / 16;
-  constexpr int A_CH = BM * 8 / 256;
-  constexpr int B_CH = BN * 8 / 256;
+  constexpr int ROWS = BM + NB * BN;   // LDS rows per stage: A tile, then the B tile(s)
+  constexpr int INS = ROWS / 8;        // 1 KiB wave-loads per stage (8 rows each)
+  constexpr int IPW = INS / 4;         // per wave
+  constexpr int STAGE_BYTES = ROWS * BK * 2;
+  // As many stages as fit in 80 KiB (two work-groups per CU share its 160 KiB),
+  // at least three; BM >= 128 runs one work-group per CU with four stages.
+  constexpr int STAGES = BM >= 128 ? 4 : (81920 / STAGE_BYTES < 3 ? 3 : 81920 / STAGE_BYTES);
   static_assert(WM * WN == 4, "4 waves per work-group");
-  static_assert(TM >= 1 && TN >= 1 && A_CH >= 1 && B_CH >= 1, "tile too small");
+  static_assert(TM >= 1 && TN >= 1 && INS % 4 == 0, "tile shape");
+  static_assert((STAGES - 2) * IPW < 64, "vmcnt range");
 
-  __shared__ __attribute__((aligned(16))) uint16_t smA[2][BM * LDK];
-  __shared__ __attribute__((aligned(16))) uint16_t smB[2][NB][BN * LDK];
+  // Ring of STAGES buffers filled by direct global->LDS loads: lane l of a
+  // wave-load writes the 16 bytes at slot base + l. Slot s of a stage holds
+  // row s >> 3, 16-byte chunk (s & 7) ^ ((row >> 1) & 7) of the tile, so the 16
+  // rows of an MFMA fragment read fall on distinct bank groups.
+  __shared__ __attribute__((aligned(16))) uint16_t sm[STAGES][ROWS * BK];
 
   const int t = xcd_remap(blockIdx.x, gridDim.x);
   const int split = t % p.splits;
@@ -103,58 +128,35 @@ __global__ __launch_bounds__(256, 2) void gemm_nt_kernel(GemmParams p) {
   const int r = lane & 15, qg = lane >> 4;
   const int wm = wave / WN, wn = wave % WN;
 
-  // Per-thread global source rows (fixed over k).
-  const uint16_t* a_src[A_CH];
+  // Global source of each of this lane's wave-loads (fixed over k). Rows past
+  // the tile (A rows >= row1, weight rows >= N) read a valid row instead; their
+  // products land in output rows/columns that are never stored.
+  const uint16_t* src[IPW];
 #pragma unroll
-  for (int i = 0; i < A_CH; ++i) {
-    const int c = tid + i * 256;
-    const int row = row0 + (c >> 3);
-    const int col = (c & 7) * 8;
-    if (row < row1) {
-      const int src = p.gather ? p.gather[row] / p.gather_div : row;
-      a_src[i] = p.A + (size_t)src * p.lda + kb + col;
+  for (int j = 0; j < IPW; ++j) {
+    const int slot = (wave + 4 * j) * 64 + lane;
+    const int row = slot >> 3;
+    const int ch = (slot & 7) ^ ((row >> 1) & 7);
+    const uint16_t* base;
+    if (row < BM) {
+      const int g = (row0 + row < row1) ? row0 + row : row0;
+      const int srow = p.gather ? p.gather[g] / p.gather_div : g;
+      base = p.A + (size_t)srow * p.lda;
     } else {
-      a_src[i] = nullptr;
+      const int rb = row - BM;
+      const int nb = rb / BN;
+      const int n = min(n0 + (rb - nb * BN), p.N - 1);
+      base = ((DUAL && nb) ? p.B1 : p.B0) + (size_t)expert * p.b_expert_stride + (size_t)n * p.ldb;
     }
-  }
-  const uint16_t* b_src[NB][B_CH];
-#pragma unroll
-  for (int i = 0; i < B_CH; ++i) {
-    const int c = tid + i * 256;
-    const int n = n0 + (c >> 3);
-    const int col = (c & 7) * 8;
-    const size_t off = (size_t)expert * p.b_expert_stride + (size_t)n * p.ldb + kb + col;
-    b_src[0][i] = (n < p.N) ? p.B0 + off : nullptr;
-    if (DUAL) b_src[NB - 1][i] = (n < p.N) ? p.B1 + off : nullptr;
+    src[j] = base + kb + ch * 8;
   }
 
-  uint4 ra[A_CH], rb[NB][B_CH];
-  auto load_global = [&](int kt) {
-    const int ko = kt * BK;
-#pragma unroll
-    for (int i = 0; i < A_CH; ++i)
-      ra[i] = a_src[i] ? *reinterpret_cast<const uint4*>(a_src[i] + ko) : make_uint4(0, 0, 0, 0);
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb)
-#pragma unroll
-      for (int i = 0; i < B_CH; ++i)
-        rb[nb][i] = b_src[nb][i] ? *reinterpret_cast<const uint4*>(b_src[nb][i] + ko)
-                                 : make_uint4(0, 0, 0, 0);
-  };
-  auto store_lds = [&](int buf) {
-#pragma unroll
-    for (int i = 0; i < A_CH; ++i) {
-      const int c = tid + i * 256;
-      *reinterpret_cast<uint4*>(&smA[buf][(c >> 3) * LDK + (c & 7) * 8]) = ra[i];
-    }
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb)
-#pragma unroll
-      for (int i = 0; i < B_CH; ++i) {
-        const int c = tid + i * 256;
-        *reinterpret_cast<uint4*>(&smB[buf][nb][(c >> 3) * LDK + (c & 7) * 8]) = rb[nb][i];
-      }
-  };
+#define AFLEX_GEMM_ISSUE(SM, KT)                                                          \
+  do {                                                                                   \
+    const int ko_ = min(KT, nk - 1) * BK;                                                \
+    _Pragma("unroll") for (int j = 0; j < IPW; ++j)                                      \
+        lds_dma16(src[j] + ko_, lds_offset(SM + (wave + 4 * j) * 512));                  \
+  } while (0)
 
   f32x4 acc[NB][TM][TN];
 #pragma unroll
@@ -164,27 +166,23 @@ __global__ __launch_bounds__(256, 2) void gemm_nt_kernel(GemmParams p) {
 #pragma unroll
       for (int j = 0; j < TN; ++j) acc[nb][i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  if (nk > 0) {
-    load_global(0);
-    store_lds(0);
-    __syncthreads();
-  }
-  for (int kt = 0; kt < nk; ++kt) {
-    const int buf = kt & 1;
-    if (kt + 1 < nk) load_global(kt + 1);
+  auto compute = [&](const uint16_t* sm) {
 #pragma unroll
     for (int kk = 0; kk < BK / 32; ++kk) {
+      const int ch = kk * 4 + qg;  // logical 16-byte chunk this lane feeds
       bf16x8 af[TM], bfr[NB][TN];
 #pragma unroll
-      for (int i = 0; i < TM; ++i)
-        af[i] = *reinterpret_cast<const bf16x8*>(
-            &smA[buf][(wm * WTM + i * 16 + r) * LDK + kk * 32 + qg * 8]);
+      for (int i = 0; i < TM; ++i) {
+        const int R = wm * WTM + i * 16 + r;
+        af[i] = *reinterpret_cast<const bf16x8*>(&sm[R * BK + ((ch ^ ((R >> 1) & 7)) << 3)]);
+      }
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
-        for (int j = 0; j < TN; ++j)
-          bfr[nb][j] = *reinterpret_cast<const bf16x8*>(
-              &smB[buf][nb][(wn * WTN + j * 16 + r) * LDK + kk * 32 + qg * 8]);
+        for (int j = 0; j < TN; ++j) {
+          const int R = BM + nb * BN + wn * WTN + j * 16 + r;
+          bfr[nb][j] = *reinterpret_cast<const bf16x8*>(&sm[R * BK + ((ch ^ ((R >> 1) & 7)) << 3)]);
+        }
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
@@ -193,9 +191,32 @@ __global__ __launch_bounds__(256, 2) void gemm_nt_kernel(GemmParams p) {
           for (int j = 0; j < TN; ++j)
             acc[nb][i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bfr[nb][j], acc[nb][i][j], 0, 0, 0);
     }
-    if (kt + 1 < nk) store_lds(buf ^ 1);
-    __syncthreads();
+  };
+
+  // Before reading stage kt: vmcnt((STAGES-2)*IPW) means this wave's loads of
+  // kt have landed while the STAGES-2 newer stages may still be in flight; the
+  // barrier publishes every wave's loads of kt and frees the buffer read in the
+  // previous step, which then receives k-step kt+STAGES-1. Prefetches past the
+  // last k-step re-read it (clamped index), so every step issues the same
+  // number of loads and the count stays exact.
+  constexpr int kWait = (STAGES - 2) * IPW;
+  constexpr int kWaitImm = (kWait & 15) | ((kWait >> 4) << 14) | (0x7 << 4) | (0xF << 8);
+  if (nk > 0) {
+#pragma unroll
+    for (int st = 0; st < STAGES - 1; ++st) AFLEX_GEMM_ISSUE(sm[st], st);
+    int cur = 0;
+    for (int kt = 0; kt < nk; ++kt) {
+      __builtin_amdgcn_s_waitcnt(kWaitImm);
+      __syncthreads();
+      const int nxt = cur == 0 ? STAGES - 1 : cur - 1;  // (kt + STAGES - 1) % STAGES
+      AFLEX_GEMM_ISSUE(sm[nxt], kt + STAGES - 1);
+      compute(sm[cur]);
+      cur = cur + 1 == STAGES ? 0 : cur + 1;
+    }
+    // no load may still target LDS when the work-group retires
+    __builtin_amdgcn_s_waitcnt(0);
   }
+#undef AFLEX_GEMM_ISSUE
 
   // Epilogue: lane holds rows (4*qg + e) and column r of every 16x16 tile.
 #pragma unroll

@@ -26,15 +26,15 @@ hipError_t launch_down(int bm, bool f32_partials, const GemmParams& g, hipStream
   ProfScope ps("gemm_down", stream);
   if (f32_partials) {
     switch (bm) {
-      case 32: gemm_nt_kernel<32, kDownBN, 1, 4, false, true><<<grid, 256, 0, stream>>>(g); break;
-      case 64: gemm_nt_kernel<64, kDownBN, 2, 2, false, true><<<grid, 256, 0, stream>>>(g); break;
-      default: gemm_nt_kernel<128, kDownBN, 2, 2, false, true><<<grid, 256, 0, stream>>>(g); break;
+      case 32: gemm_nt_kernel<32, 128, 1, 4, false, true><<<grid, 256, 0, stream>>>(g); break;
+      case 64: gemm_nt_kernel<64, 128, 2, 2, false, true><<<grid, 256, 0, stream>>>(g); break;
+      default: gemm_nt_kernel<128, 128, 2, 2, false, true><<<grid, 256, 0, stream>>>(g); break;
     }
   } else {
     switch (bm) {
-      case 32: gemm_nt_kernel<32, kDownBN, 1, 4, false, false><<<grid, 256, 0, stream>>>(g); break;
-      case 64: gemm_nt_kernel<64, kDownBN, 2, 2, false, false><<<grid, 256, 0, stream>>>(g); break;
-      default: gemm_nt_kernel<128, kDownBN, 2, 2, false, false><<<grid, 256, 0, stream>>>(g); break;
+      case 32: gemm_nt_kernel<32, 128, 1, 4, false, false><<<grid, 256, 0, stream>>>(g); break;
+      case 64: gemm_nt_kernel<64, 128, 2, 2, false, false><<<grid, 256, 0, stream>>>(g); break;
+      default: gemm_nt_kernel<128, 128, 2, 2, false, false><<<grid, 256, 0, stream>>>(g); break;
     }
   }
   return hipGetLastError();

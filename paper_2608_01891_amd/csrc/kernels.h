@@ -21,5 +21,11 @@ hipError_t launch_swiglu(const aflex_ffn_args& f, void* ws, hipStream_t stream);
 // Top-k MoE FFN (moe.hip).
 size_t moe_workspace_bytes(const aflex_ffn_args& f);
 hipError_t launch_moe(const aflex_ffn_args& f, void* ws, hipStream_t stream);
+// The two halves of launch_moe: routing (depends only on the logits) and the
+// expert computation, with separate workspace blocks.
+size_t moe_route_bytes(const aflex_ffn_args& f);
+size_t moe_expert_bytes(const aflex_ffn_args& f);
+hipError_t launch_moe_route(const aflex_ffn_args& f, void* route_ws, hipStream_t stream);
+hipError_t launch_moe_experts(const aflex_ffn_args& f, void* route_ws, void* expert_ws, hipStream_t stream);
 
 }  // namespace aflex

@@ -25,8 +25,12 @@ namespace aflex {
 constexpr int kMaxK = 8;
 constexpr int kMaxE = 64;
 
+// Workspace: a routing block (ids .. num_tiles, written by the route kernel)
+// followed by the expert block (h, P). The two can live apart: the pipeline
+// keeps one routing block per microbatch and one shared expert block.
 struct MoeLayout {
-  size_t ids, wts, offsets, sorted, pos, tile_map, num_tiles, h, P, total;
+  size_t ids, wts, offsets, sorted, pos, tile_map, num_tiles, route_total;
+  size_t h, P, expert_total;
   int bm, max_tiles, down_splits, down_kps;
 };
 
@@ -35,7 +39,7 @@ static MoeLayout moe_layout(const aflex_ffn_args& f) {
   const size_t pairs = (size_t)f.T * f.k;
   L.bm = pick_bm((double)pairs / f.E);
   L.max_tiles = (int)((pairs + L.bm - 1) / L.bm) + f.E;
-  const int ntiles = (f.H + kDownBN - 1) / kDownBN;
+  const int ntiles = (f.H + down_bn(L.bm) - 1) / down_bn(L.bm);
   plan_splits(L.max_tiles * ntiles, f.I, 512, 16, &L.down_splits, &L.down_kps);
   size_t o = 0;
   auto take = [&](size_t bytes) {
@@ -50,13 +54,20 @@ static MoeLayout moe_layout(const aflex_ffn_args& f) {
   L.pos = take(pairs * 4);
   L.tile_map = take((size_t)L.max_tiles * 3 * 4);
   L.num_tiles = take(4);
+  L.route_total = o;
+  o = 0;
   L.h = take(pairs * f.I * 2);
   L.P = take((size_t)L.down_splits * pairs * f.H * 4);
-  L.total = o;
+  L.expert_total = o;
   return L;
 }
 
-size_t moe_workspace_bytes(const aflex_ffn_args& f) { return moe_layout(f).total; }
+size_t moe_route_bytes(const aflex_ffn_args& f) { return moe_layout(f).route_total; }
+size_t moe_expert_bytes(const aflex_ffn_args& f) { return moe_layout(f).expert_total; }
+size_t moe_workspace_bytes(const aflex_ffn_args& f) {
+  const MoeLayout L = moe_layout(f);
+  return L.route_total + L.expert_total;
+}
 
 __global__ __launch_bounds__(256) void moe_route_kernel(const float* __restrict__ logits, int T, int E, int k,
                                                         int bm, int32_t* ids, float* wts, int32_t* offsets,
@@ -195,27 +206,38 @@ __global__ __launch_bounds__(256) void moe_combine_kernel(const float* __restric
   *reinterpret_cast<ushort4*>(y + (size_t)t * H + c) = o;
 }
 
+hipError_t launch_moe_route(const aflex_ffn_args& f, void* route_ws, hipStream_t stream) {
+  const MoeLayout L = moe_layout(f);
+  char* w = static_cast<char*>(route_ws);
+  ProfScope ps("moe_route", stream);
+  moe_route_kernel<<<1, 256, 0, stream>>>(
+      f.router_logits, f.T, f.E, f.k, L.bm, reinterpret_cast<int32_t*>(w + L.ids),
+      reinterpret_cast<float*>(w + L.wts), reinterpret_cast<int32_t*>(w + L.offsets),
+      reinterpret_cast<int32_t*>(w + L.sorted), reinterpret_cast<int32_t*>(w + L.pos),
+      reinterpret_cast<int32_t*>(w + L.tile_map), reinterpret_cast<int32_t*>(w + L.num_tiles), f.topk_ids,
+      f.topk_w, f.expert_offsets, f.sorted_pairs);
+  return hipGetLastError();
+}
+
 hipError_t launch_moe(const aflex_ffn_args& f, void* ws, hipStream_t stream) {
   const MoeLayout L = moe_layout(f);
-  char* w = static_cast<char*>(ws);
-  int32_t* ids = reinterpret_cast<int32_t*>(w + L.ids);
-  float* wts = reinterpret_cast<float*>(w + L.wts);
-  int32_t* offsets = reinterpret_cast<int32_t*>(w + L.offsets);
-  int32_t* sorted = reinterpret_cast<int32_t*>(w + L.sorted);
-  int32_t* pos = reinterpret_cast<int32_t*>(w + L.pos);
-  int32_t* tile_map = reinterpret_cast<int32_t*>(w + L.tile_map);
-  int32_t* num_tiles = reinterpret_cast<int32_t*>(w + L.num_tiles);
-  uint16_t* h = reinterpret_cast<uint16_t*>(w + L.h);
-  float* P = reinterpret_cast<float*>(w + L.P);
-
-  {
-    ProfScope ps("moe_route", stream);
-    moe_route_kernel<<<1, 256, 0, stream>>>(f.router_logits, f.T, f.E, f.k, L.bm, ids, wts, offsets, sorted, pos,
-                                            tile_map, num_tiles, f.topk_ids, f.topk_w, f.expert_offsets,
-                                            f.sorted_pairs);
-  }
-  hipError_t e = hipGetLastError();
+  hipError_t e = launch_moe_route(f, ws, stream);
   if (e != hipSuccess) return e;
+  return launch_moe_experts(f, ws, static_cast<char*>(ws) + L.route_total, stream);
+}
+
+hipError_t launch_moe_experts(const aflex_ffn_args& f, void* route_ws, void* expert_ws, hipStream_t stream) {
+  const MoeLayout L = moe_layout(f);
+  char* w = static_cast<char*>(route_ws);
+  char* xw = static_cast<char*>(expert_ws);
+  const float* wts = reinterpret_cast<const float*>(w + L.wts);
+  const int32_t* sorted = reinterpret_cast<const int32_t*>(w + L.sorted);
+  const int32_t* pos = reinterpret_cast<const int32_t*>(w + L.pos);
+  const int32_t* tile_map = reinterpret_cast<const int32_t*>(w + L.tile_map);
+  const int32_t* num_tiles = reinterpret_cast<const int32_t*>(w + L.num_tiles);
+  uint16_t* h = reinterpret_cast<uint16_t*>(xw + L.h);
+  float* P = reinterpret_cast<float*>(xw + L.P);
+  hipError_t e;
 
   GemmParams g = {};
   g.A = f.x;
@@ -254,7 +276,7 @@ hipError_t launch_moe(const aflex_ffn_args& f, void* ws, hipStream_t stream) {
   d.tile_map = tile_map;
   d.num_mtiles = num_tiles;
   d.max_mtiles = L.max_tiles;
-  d.n_ntiles = (f.H + kDownBN - 1) / kDownBN;
+  d.n_ntiles = (f.H + down_bn(L.bm) - 1) / down_bn(L.bm);
   d.mt_major = 1;
   d.P = P;
   d.p_split_stride = pairs * f.H;
