@@ -55,7 +55,7 @@ hipError_t launch_swiglu(const aflex_ffn_args& f, void* ws, hipStream_t stream) 
   g.splits = 1;
   g.M = f.T;
   g.max_mtiles = (f.T + pl.bm - 1) / pl.bm;
-  g.n_ntiles = (f.I + kGateBN - 1) / kGateBN;
+  g.n_ntiles = (f.I + gate_bn(pl.bm) - 1) / gate_bn(pl.bm);
   g.mt_major = 0;
   g.C = h;
   g.ldc = f.I;

@@ -6,10 +6,13 @@
 
 namespace aflex {
 
-constexpr int kGateBN = 64;  // output columns per gate/up tile (x2 weight rows)
+// Output columns per gate/up tile (x2 weight rows) and per down tile.
+inline int gate_bn(int bm) { return bm >= 256 ? 128 : 64; }
 
-constexpr int kDownBN = 128;  // output columns per down tile
-inline int down_bn(int) { return kDownBN; }
+inline int down_bn(int) { return 128; }
+// Work-groups the down GEMM's split-K aims for: the 256-row tiles run one
+// work-group per CU, so one round of the chip; smaller tiles two per CU.
+inline int down_target(int bm) { return bm >= 256 ? 256 : 512; }
 
 struct FfnPlan {
   int bm;           // rows per m-tile: 32, 64 or 128
@@ -17,10 +20,14 @@ struct FfnPlan {
   int down_kps;     // k elements per split (multiple of 64)
 };
 
-inline int pick_bm(double rows_per_tile_group) {
-  if (rows_per_tile_group * 1.3 <= 32) return 32;
-  if (rows_per_tile_group * 1.3 <= 64) return 64;
-  return 128;
+// Rows per m-tile for grouped GEMMs with the given average rows per expert:
+// large enough that a typical expert needs one tile (its weights are then
+// streamed once), up to the MFMA-bound 256-row shape.
+inline int pick_bm(double rows_per_expert) {
+  if (rows_per_expert * 1.3 <= 32) return 32;
+  if (rows_per_expert * 1.3 <= 64) return 64;
+  if (rows_per_expert <= 160) return 128;
+  return 256;
 }
 
 // Split K so that the down GEMM has about `target` work-groups, keeping at
@@ -39,10 +46,10 @@ inline void plan_splits(int base_tiles, int K, int target, int min_steps, int* s
 
 inline FfnPlan plan_dense(int T, int H, int I) {
   FfnPlan pl;
-  pl.bm = T <= 32 ? 32 : (T <= 64 ? 64 : 128);
+  pl.bm = T <= 32 ? 32 : (T <= 64 ? 64 : (T <= 128 ? 128 : 256));
   const int mtiles = (T + pl.bm - 1) / pl.bm;
   const int ntiles = (H + down_bn(pl.bm) - 1) / down_bn(pl.bm);
-  plan_splits(mtiles * ntiles, I, 512, 8, &pl.down_splits, &pl.down_kps);
+  plan_splits(mtiles * ntiles, I, down_target(pl.bm), 8, &pl.down_splits, &pl.down_kps);
   return pl;
 }
 

@@ -27,6 +27,8 @@
 // work-groups beyond the map's device-side count exit at once, so the grid is
 // sized for the worst case without a host synchronisation.
 #pragma once
+#include <type_traits>
+
 #include "common.h"
 
 namespace aflex {
@@ -74,27 +76,36 @@ __device__ __forceinline__ int xcd_remap(int w, int nwg) {
   return (x < rem ? x * (q + 1) : rem * (q + 1) + (x - rem) * q) + j;
 }
 
-template <int BM, int BN, int WM, int WN, bool DUAL, bool OUT_F32>
-__global__ __launch_bounds__(256, BM >= 128 ? 1 : 2) void gemm_nt_kernel(GemmParams p) {
-  constexpr int BK = 64;  // one LDS row = 64 bf16 = 128 B = 8 chunks of 16 B
+// BM x BN output tile, WM x WN waves (each a (BM/WM) x (BN/WN) sub-tile of
+// MS x MS MFMA tiles: v_mfma_f32_16x16x32_bf16 or v_mfma_f32_32x32x16_bf16),
+// BK-wide k-steps, LDS_BYTES of LDS per work-group (the ring has as many
+// stages as fit; 80 KiB lets two work-groups share a CU). The 32x32 MFMA
+// sustains a higher issue rate and serves the MFMA-bound tiles.
+template <int BM, int BN, int WM, int WN, int BK, int MS, bool DUAL, bool OUT_F32, int LDS_BYTES>
+__global__ __launch_bounds__(64 * WM * WN, LDS_BYTES > 81920 ? 1 : 2) void gemm_nt_kernel(GemmParams p) {
+  constexpr int NW = WM * WN;
   constexpr int NB = DUAL ? 2 : 1;
   constexpr int WTM = BM / WM, WTN = BN / WN;
-  constexpr int TM = WTM / 16, TN = WTN / 16;
-  constexpr int ROWS = BM + NB * BN;   // LDS rows per stage: A tile, then the B tile(s)
-  constexpr int INS = ROWS / 8;        // 1 KiB wave-loads per stage (8 rows each)
-  constexpr int IPW = INS / 4;         // per wave
+  constexpr int TM = WTM / MS, TN = WTN / MS;
+  using Acc = typename std::conditional<MS == 16, f32x4, f32x16>::type;
+  constexpr int NACC = MS == 16 ? 4 : 16;
+  constexpr int CPR = BK / 8;           // 16-byte chunks per LDS row
+  constexpr int WIN = 128 / BK;         // rows per 256-byte bank window
+  constexpr int ROWS = BM + NB * BN;    // LDS rows per stage: A tile, then the B tile(s)
+  constexpr int INS = ROWS * CPR / 64;  // 1 KiB wave-loads per stage
+  constexpr int IPW = INS / NW;         // per wave
   constexpr int STAGE_BYTES = ROWS * BK * 2;
-  // As many stages as fit in 80 KiB (two work-groups per CU share its 160 KiB),
-  // at least three; BM >= 128 runs one work-group per CU with four stages.
-  constexpr int STAGES = BM >= 128 ? 4 : (81920 / STAGE_BYTES < 3 ? 3 : 81920 / STAGE_BYTES);
-  static_assert(WM * WN == 4, "4 waves per work-group");
-  static_assert(TM >= 1 && TN >= 1 && INS % 4 == 0, "tile shape");
-  static_assert((STAGES - 2) * IPW < 64, "vmcnt range");
+  constexpr int STAGES = LDS_BYTES / STAGE_BYTES;
+  static_assert(BK == 32 || BK == 64, "k-step");
+  static_assert(MS == 16 || MS == 32, "MFMA shape");
+  static_assert(TM >= 1 && TN >= 1 && INS % NW == 0, "tile shape");
+  static_assert(STAGES >= 2 && (STAGES - 2) * IPW < 64, "stages");
 
   // Ring of STAGES buffers filled by direct global->LDS loads: lane l of a
   // wave-load writes the 16 bytes at slot base + l. Slot s of a stage holds
-  // row s >> 3, 16-byte chunk (s & 7) ^ ((row >> 1) & 7) of the tile, so the 16
-  // rows of an MFMA fragment read fall on distinct bank groups.
+  // row s / CPR, 16-byte chunk (s % CPR) ^ swz(row) of the tile, with
+  // swz(row) = (row / WIN) % CPR, so the 16 rows of an MFMA fragment read fall
+  // on distinct bank groups.
   __shared__ __attribute__((aligned(16))) uint16_t sm[STAGES][ROWS * BK];
 
   const int t = xcd_remap(blockIdx.x, gridDim.x);
@@ -125,7 +136,8 @@ __global__ __launch_bounds__(256, BM >= 128 ? 1 : 2) void gemm_nt_kernel(GemmPar
 
   const int tid = threadIdx.x;
   const int wave = tid >> 6, lane = tid & 63;
-  const int r = lane & 15, qg = lane >> 4;
+  // MFMA operand lane roles: row/column r of the tile, k-slice g (8 wide).
+  const int r = lane & (MS - 1), qg = lane / MS;
   const int wm = wave / WN, wn = wave % WN;
 
   // Global source of each of this lane's wave-loads (fixed over k). Rows past
@@ -134,9 +146,9 @@ __global__ __launch_bounds__(256, BM >= 128 ? 1 : 2) void gemm_nt_kernel(GemmPar
   const uint16_t* src[IPW];
 #pragma unroll
   for (int j = 0; j < IPW; ++j) {
-    const int slot = (wave + 4 * j) * 64 + lane;
-    const int row = slot >> 3;
-    const int ch = (slot & 7) ^ ((row >> 1) & 7);
+    const int slot = (wave + NW * j) * 64 + lane;
+    const int row = slot / CPR;
+    const int ch = (slot % CPR) ^ ((row / WIN) % CPR);
     const uint16_t* base;
     if (row < BM) {
       const int g = (row0 + row < row1) ? row0 + row : row0;
@@ -155,79 +167,108 @@ __global__ __launch_bounds__(256, BM >= 128 ? 1 : 2) void gemm_nt_kernel(GemmPar
   do {                                                                                   \
     const int ko_ = min(KT, nk - 1) * BK;                                                \
     _Pragma("unroll") for (int j = 0; j < IPW; ++j)                                      \
-        lds_dma16(src[j] + ko_, lds_offset(SM + (wave + 4 * j) * 512));                  \
+        lds_dma16(src[j] + ko_, lds_offset(SM + (wave + NW * j) * 512));                 \
   } while (0)
 
-  f32x4 acc[NB][TM][TN];
+  Acc acc[NB][TM][TN];
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
     for (int i = 0; i < TM; ++i)
 #pragma unroll
-      for (int j = 0; j < TN; ++j) acc[nb][i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+      for (int j = 0; j < TN; ++j)
+#pragma unroll
+        for (int e = 0; e < NACC; ++e) acc[nb][i][j][e] = 0.f;
 
-  auto compute = [&](const uint16_t* sm) {
-#pragma unroll
-    for (int kk = 0; kk < BK / 32; ++kk) {
-      const int ch = kk * 4 + qg;  // logical 16-byte chunk this lane feeds
-      bf16x8 af[TM], bfr[NB][TN];
-#pragma unroll
-      for (int i = 0; i < TM; ++i) {
-        const int R = wm * WTM + i * 16 + r;
-        af[i] = *reinterpret_cast<const bf16x8*>(&sm[R * BK + ((ch ^ ((R >> 1) & 7)) << 3)]);
-      }
-#pragma unroll
-      for (int nb = 0; nb < NB; ++nb)
-#pragma unroll
-        for (int j = 0; j < TN; ++j) {
-          const int R = BM + nb * BN + wn * WTN + j * 16 + r;
-          bfr[nb][j] = *reinterpret_cast<const bf16x8*>(&sm[R * BK + ((ch ^ ((R >> 1) & 7)) << 3)]);
-        }
-#pragma unroll
-      for (int nb = 0; nb < NB; ++nb)
-#pragma unroll
-        for (int i = 0; i < TM; ++i)
-#pragma unroll
-          for (int j = 0; j < TN; ++j)
-            acc[nb][i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bfr[nb][j], acc[nb][i][j], 0, 0, 0);
-    }
-  };
+  constexpr int KC = MS == 16 ? 32 : 16;  // k per MFMA
+  constexpr int CPS = BK / KC;             // MFMA k-chunks per stage
+  const int nchunks = nk * CPS;
 
-  // Before reading stage kt: vmcnt((STAGES-2)*IPW) means this wave's loads of
-  // kt have landed while the STAGES-2 newer stages may still be in flight; the
-  // barrier publishes every wave's loads of kt and frees the buffer read in the
-  // previous step, which then receives k-step kt+STAGES-1. Prefetches past the
-  // last k-step re-read it (clamped index), so every step issues the same
-  // number of loads and the count stays exact.
+  // Fragments of k-chunk C (of stage C / CPS) into registers FA, FB.
+#define AFLEX_GEMM_READ(FA, FB, C)                                                         \
+  do {                                                                                    \
+    const int kt_ = (C) / CPS;                                                            \
+    const uint16_t* smp_ = sm[kt_ % STAGES];                                              \
+    const int ch_ = ((C) - kt_ * CPS) * (KC / 8) + qg;                                    \
+    _Pragma("unroll") for (int i = 0; i < TM; ++i) {                                      \
+      const int R = wm * WTM + i * MS + r;                                                \
+      FA[i] = *reinterpret_cast<const bf16x8*>(&smp_[R * BK + ((ch_ ^ ((R / WIN) % CPR)) << 3)]); \
+    }                                                                                     \
+    _Pragma("unroll") for (int nb = 0; nb < NB; ++nb)                                     \
+        _Pragma("unroll") for (int j = 0; j < TN; ++j) {                                  \
+      const int R = BM + nb * BN + wn * WTN + j * MS + r;                                 \
+      FB[nb][j] = *reinterpret_cast<const bf16x8*>(&smp_[R * BK + ((ch_ ^ ((R / WIN) % CPR)) << 3)]); \
+    }                                                                                     \
+  } while (0)
+#define AFLEX_GEMM_MMA(FA, FB)                                                             \
+  do {                                                                                    \
+    _Pragma("unroll") for (int nb = 0; nb < NB; ++nb)                                     \
+        _Pragma("unroll") for (int i = 0; i < TM; ++i)                                    \
+            _Pragma("unroll") for (int j = 0; j < TN; ++j) {                              \
+      if constexpr (MS == 16)                                                             \
+        acc[nb][i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(FA[i], FB[nb][j], acc[nb][i][j], 0, 0, 0); \
+      else                                                                                \
+        acc[nb][i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(FA[i], FB[nb][j], acc[nb][i][j], 0, 0, 0); \
+    }                                                                                     \
+  } while (0)
+  // Make stage KT1 readable: vmcnt((STAGES-2)*IPW) means this wave's loads of
+  // KT1 have landed while the STAGES-2 newer stages may still be in flight; the
+  // barrier (which first drains this wave's LDS reads) publishes every wave's
+  // loads of KT1 and guarantees stage KT1-1 is no longer read, so its buffer
+  // receives k-step KT1+STAGES-1. Prefetches past the last k-step re-read it
+  // (clamped index), so every stage issues the same number of loads and the
+  // count stays exact.
   constexpr int kWait = (STAGES - 2) * IPW;
   constexpr int kWaitImm = (kWait & 15) | ((kWait >> 4) << 14) | (0x7 << 4) | (0xF << 8);
+#define AFLEX_GEMM_STAGE(KT1)                                                              \
+  do {                                                                                    \
+    __builtin_amdgcn_s_waitcnt(kWaitImm);                                                 \
+    __syncthreads();                                                                      \
+    AFLEX_GEMM_ISSUE(sm[((KT1) + STAGES - 1) % STAGES], (KT1) + STAGES - 1);              \
+  } while (0)
+
+  // Software pipeline over k-chunks: the fragments of chunk c+1 are read while
+  // the MFMAs of chunk c run; a stage boundary's wait and barrier sit between
+  // the two, behind the in-flight MFMAs.
   if (nk > 0) {
+    bf16x8 fa0[TM], fb0[NB][TN], fa1[TM], fb1[NB][TN];
 #pragma unroll
     for (int st = 0; st < STAGES - 1; ++st) AFLEX_GEMM_ISSUE(sm[st], st);
-    int cur = 0;
-    for (int kt = 0; kt < nk; ++kt) {
-      __builtin_amdgcn_s_waitcnt(kWaitImm);
-      __syncthreads();
-      const int nxt = cur == 0 ? STAGES - 1 : cur - 1;  // (kt + STAGES - 1) % STAGES
-      AFLEX_GEMM_ISSUE(sm[nxt], kt + STAGES - 1);
-      compute(sm[cur]);
-      cur = cur + 1 == STAGES ? 0 : cur + 1;
+    AFLEX_GEMM_STAGE(0);
+    AFLEX_GEMM_READ(fa0, fb0, 0);
+    for (int c = 0; c < nchunks; c += 2) {
+      if (c + 1 < nchunks) {
+        if ((c + 1) % CPS == 0) AFLEX_GEMM_STAGE((c + 1) / CPS);
+        AFLEX_GEMM_READ(fa1, fb1, c + 1);
+      }
+      AFLEX_GEMM_MMA(fa0, fb0);
+      if (c + 1 >= nchunks) break;
+      if (c + 2 < nchunks) {
+        if ((c + 2) % CPS == 0) AFLEX_GEMM_STAGE((c + 2) / CPS);
+        AFLEX_GEMM_READ(fa0, fb0, c + 2);
+      }
+      AFLEX_GEMM_MMA(fa1, fb1);
     }
     // no load may still target LDS when the work-group retires
     __builtin_amdgcn_s_waitcnt(0);
   }
+#undef AFLEX_GEMM_READ
+#undef AFLEX_GEMM_MMA
+#undef AFLEX_GEMM_STAGE
 #undef AFLEX_GEMM_ISSUE
 
-  // Epilogue: lane holds rows (4*qg + e) and column r of every 16x16 tile.
+  // Epilogue. 16x16 tiles: accumulator e of a lane is row 4 g + e, column r.
+  // 32x32 tiles: row (e / 4) * 8 + 4 g + e % 4, column r.
 #pragma unroll
   for (int i = 0; i < TM; ++i) {
 #pragma unroll
     for (int j = 0; j < TN; ++j) {
-      const int col = n0 + wn * WTN + j * 16 + r;
+      const int col = n0 + wn * WTN + j * MS + r;
       if (col >= p.N) continue;
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int row = row0 + wm * WTM + i * 16 + 4 * qg + e;
+      for (int e = 0; e < NACC; ++e) {
+        const int er = MS == 16 ? 4 * qg + e : (e >> 2) * 8 + 4 * qg + (e & 3);
+        const int row = row0 + wm * WTM + i * MS + er;
         if (row >= row1) continue;
         if (OUT_F32) {
           p.P[(size_t)split * p.p_split_stride + (size_t)row * p.ldp + col] = acc[0][i][j][e];

@@ -40,7 +40,7 @@ static MoeLayout moe_layout(const aflex_ffn_args& f) {
   L.bm = pick_bm((double)pairs / f.E);
   L.max_tiles = (int)((pairs + L.bm - 1) / L.bm) + f.E;
   const int ntiles = (f.H + down_bn(L.bm) - 1) / down_bn(L.bm);
-  plan_splits(L.max_tiles * ntiles, f.I, 512, 16, &L.down_splits, &L.down_kps);
+  plan_splits(L.max_tiles * ntiles, f.I, down_target(L.bm), 16, &L.down_splits, &L.down_kps);
   size_t o = 0;
   auto take = [&](size_t bytes) {
     size_t at = o;
@@ -255,7 +255,7 @@ hipError_t launch_moe_experts(const aflex_ffn_args& f, void* route_ws, void* exp
   g.tile_map = tile_map;
   g.num_mtiles = num_tiles;
   g.max_mtiles = L.max_tiles;
-  g.n_ntiles = (f.I + kGateBN - 1) / kGateBN;
+  g.n_ntiles = (f.I + gate_bn(L.bm) - 1) / gate_bn(L.bm);
   g.mt_major = 1;
   g.C = h;
   g.ldc = f.I;

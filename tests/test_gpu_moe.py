@@ -24,7 +24,8 @@ def _check_routing(r, logits, k, E):
 
 
 @pytest.mark.parametrize("T,H,I,E,k", [(37, 128, 192, 6, 3), (1, 64, 64, 8, 2), (100, 256, 320, 8, 2),
-                                       (9, 128, 128, 4, 4), (12, 128, 64, 1, 1), (300, 192, 256, 16, 8)])
+                                       (9, 128, 128, 4, 4), (12, 128, 64, 1, 1), (300, 192, 256, 16, 8),
+                                       (400, 128, 192, 2, 1), (700, 192, 128, 3, 2)])
 def test_small_shapes(gpu_lib, T, H, I, E, k):
     x, w, logits = synth.custom_ffn(60 + T, T, H, I, E=E)
     y, r = aflex.moe_ffn(x.to(DEV), w.to(DEV), logits.to(DEV), k, routing=True)
