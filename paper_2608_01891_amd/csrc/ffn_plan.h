@@ -25,7 +25,7 @@ struct FfnPlan {
 // streamed once), up to the MFMA-bound 256-row shape.
 inline int pick_bm(double rows_per_expert) {
   if (rows_per_expert * 1.3 <= 32) return 32;
-  if (rows_per_expert * 1.3 <= 64) return 64;
+  if (rows_per_expert <= 72) return 64;
   if (rows_per_expert <= 160) return 128;
   return 256;
 }

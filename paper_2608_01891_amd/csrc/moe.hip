@@ -256,7 +256,7 @@ hipError_t launch_moe_experts(const aflex_ffn_args& f, void* route_ws, void* exp
   g.num_mtiles = num_tiles;
   g.max_mtiles = L.max_tiles;
   g.n_ntiles = (f.I + gate_bn(L.bm) - 1) / gate_bn(L.bm);
-  g.mt_major = 1;
+  g.mt_major = 0;  // an expert's m-tiles are adjacent: overflow tiles re-read its weights from L2
   g.C = h;
   g.ldc = f.I;
   e = launch_gate_up(L.bm, g, stream);
@@ -277,7 +277,7 @@ hipError_t launch_moe_experts(const aflex_ffn_args& f, void* route_ws, void* exp
   d.num_mtiles = num_tiles;
   d.max_mtiles = L.max_tiles;
   d.n_ntiles = (f.H + down_bn(L.bm) - 1) / down_bn(L.bm);
-  d.mt_major = 1;
+  d.mt_major = 0;
   d.P = P;
   d.p_split_stride = pairs * f.H;
   d.ldp = f.H;
