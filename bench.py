@@ -119,19 +119,35 @@ def main():
     def step(m=mbs):
         aflex.af_pipeline_step(a, f, logits, k, m, y=y, stream_a=sa, stream_f=sf, ws=pws, join=False)
 
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-
     if args.counters_pass:
-        for _ in range(args.steps):
-            step()
+        # Counter collection serialises dispatches; it runs the FFN stage's kernels
+        # at the pipeline's microbatch shape on one stream (no cross-stream waits),
+        # then a 1 GiB device copy that calibrates the counters.
+        ws1 = aflex.Workspace()
+        out = torch.empty(a.B, a.Hq, a.D, dtype=torch.bfloat16, device=dev)
+        off = 0
+        for n in mbs:
+            am = synth.AttnInputs(q=a.q[off:off + n], k_cache=a.k_cache, v_cache=a.v_cache,
+                                  block_table=a.block_table[off:off + n],
+                                  context_lens=a.context_lens[off:off + n], B=n, Hq=a.Hq,
+                                  Hkv=a.Hkv, D=a.D, block_size=16, max_blocks=a.max_blocks,
+                                  num_blocks=a.num_blocks, max_context_len=a.max_context_len)
+            aflex.attn_decode(am, out=out[off:off + n], ws=ws1)
+            for _ in range(args.steps):
+                aflex.moe_ffn(out[off:off + n].view(n, H), f, logits[off:off + n], k,
+                              y=y[off:off + n], ws=ws1)
+            off += n
+            print(f"counters pass: microbatch of {n} done", flush=True)
         src = torch.empty(1 << 29, dtype=torch.int16, device=dev)  # 1 GiB
         dst = torch.empty_like(src)
         dst.copy_(src)
         torch.cuda.synchronize()
         print(json.dumps({"counters_pass": True, "steps": args.steps, "copy_bytes": 2 * src.numel()}))
         return
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
 
     t0 = time.perf_counter()
     for _ in range(args.steps):
