@@ -303,7 +303,32 @@ def main():
             "hbm_frac": round(abytes / (ms * 1e-3) / PEAK_HBM, 4), "bytes": abytes,
             "tflops": round(aflops / (ms * 1e-3) / 1e12, 2), "tok_per_s": round(wq.B / (ms * 1e-3), 1),
             "kernels": {kname: round(v[1] / v[0], 5) for kname, v in kp.items()}}
-        del copies, wq
+        # The whole attention stage of a Qwen3 decode layer: KV append of the new
+        # token, attention, output projection [64, 8192] x [5120, 8192]^T.
+        kn = synth.normal_tensor(1, 40, (wq.B, wq.Hkv, wq.D), device=dev)
+        vn = synth.normal_tensor(1, 41, (wq.B, wq.Hkv, wq.D), device=dev)
+        w_o = synth.normal_tensor(1, 42, (5120, wq.Hq * wq.D), scale=0.02, device=dev)
+        y_o = torch.empty(wq.B, 5120, dtype=torch.bfloat16, device=dev)
+        it[0] = 0
+
+        def run_stage():
+            c = copies[it[0] % 3]
+            aflex.kv_append(c, kn, vn)
+            aflex.attn_decode(c, out=outq)
+            aflex.linear(outq.view(wq.B, -1), w_o, y=y_o)
+            it[0] += 1
+        for _ in range(3):
+            run_stage()
+        aflex.profile_start(["kv_append", "attn_split", "attn_merge", "gemm_down", "splitk_reduce"])
+        ms = timed(run_stage, 30)
+        kp = aflex.profile_stop()
+        sbytes = abytes + w_o.numel() * 2 + 2 * wq.B * 5120 * 2 + 2 * kn.numel() * 2
+        ops["attention_stage_qwen3_B64"] = {
+            "ms": round(ms, 5), "GB_per_s": round(sbytes / (ms * 1e-3) / 1e9, 1),
+            "hbm_frac": round(sbytes / (ms * 1e-3) / PEAK_HBM, 4), "bytes": sbytes,
+            "tok_per_s": round(wq.B / (ms * 1e-3), 1),
+            "kernels": {kname: round(v[1] / v[0], 5) for kname, v in kp.items()}}
+        del copies, wq, w_o
 
         # Full-batch long-context attention of the pipeline workload
         outl = torch.empty(B, a.Hq, a.D, dtype=torch.bfloat16, device=dev)

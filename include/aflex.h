@@ -144,13 +144,52 @@ aflex_status aflex_af_pipeline_step(const aflex_attn_args *attn, const aflex_ffn
                                     aflex_stream stream_a, aflex_stream stream_f);
 
 /* ------------------------------------------------------------------------ */
+/* Steps either side of decode attention in the attention stage.            */
+/* KV append: each decode step adds the new token's key and value to the    */
+/* growing cache before attention reads it (section 1; section 2). With the */
+/* new token counted in context_lens, it is written at j = ctx_b - 1:        */
+/*   k_cache[block_table[b][j / 16]][g][j % 16][:] = k_new[b][g][:]          */
+/*   v_cache[block_table[b][j / 16]][g][:][j % 16] = v_new[b][g][:]          */
+/* Nothing is written for ctx_b <= 0, for j beyond the table's capacity or   */
+/* for block ids outside [0, num_blocks). Pools are updated in place.        */
+/* ------------------------------------------------------------------------ */
+typedef struct aflex_kv_append_args {
+  const aflex_bf16 *k_new;     /* [B, Hkv, D] */
+  const aflex_bf16 *v_new;     /* [B, Hkv, D] */
+  aflex_bf16 *k_cache;         /* [num_blocks, Hkv, block_size, D] (written) */
+  aflex_bf16 *v_cache;         /* [num_blocks, Hkv, D, block_size] (written) */
+  const int32_t *block_table;  /* [B, max_blocks_per_seq] */
+  const int32_t *context_lens; /* [B], including the new token */
+  int32_t B, Hkv, D;
+  int32_t block_size;          /* must be 16 */
+  int32_t max_blocks_per_seq, num_blocks;
+} aflex_kv_append_args;
+
+/* Supported: D in {64, 128}, block_size == 16. No workspace. */
+aflex_status aflex_kv_append(const aflex_kv_append_args *a, aflex_stream stream);
+
+/* Linear layer y = x W^T in bf16 with fp32 accumulation: the output           */
+/* projection that brings the attention output back to the hidden size        */
+/* before it crosses the A/F boundary (section 4.3).                           */
+typedef struct aflex_linear_args {
+  const aflex_bf16 *x;  /* [T, K] */
+  const aflex_bf16 *w;  /* [N, K] (out_features, in_features) */
+  aflex_bf16 *y;        /* [T, N] */
+  int32_t T, K, N;      /* K and N multiples of 64 */
+} aflex_linear_args;
+
+aflex_status aflex_linear_workspace(const aflex_linear_args *l, size_t *bytes);
+aflex_status aflex_linear(const aflex_linear_args *l, void *workspace, size_t workspace_bytes,
+                          aflex_stream stream);
+
+/* ------------------------------------------------------------------------ */
 /* Per-kernel timing, the single-GPU analogue of the paper's per-operator     */
 /* latency profiling (section 4.1; section 5, "Profiling module"). Between    */
 /* aflex_profile_start and aflex_profile_stop, every library kernel whose     */
 /* name is in the comma-separated list `kernels` (NULL or "" = all) is        */
 /* bracketed by two HIP events on the stream it is launched on. Kernel names: */
 /* attn_split, attn_merge, gemm_gate_up, gemm_down, splitk_reduce, moe_route, */
-/* moe_combine. aflex_profile_stop waits for those events and writes one line */
+/* moe_combine, kv_append. aflex_profile_stop waits for those events and writes one line */
 /* per kernel into `report` (host buffer of `len` bytes, truncated to fit):   */
 /*   "<name> <launches> <total_ms> <min_ms> <max_ms>
 "                      */

@@ -38,6 +38,17 @@ class FfnArgs(ctypes.Structure):
                 ("T", _i), ("H", _i), ("I", _i), ("E", _i), ("k", _i)]
 
 
+class KvAppendArgs(ctypes.Structure):
+    _fields_ = [("k_new", _p), ("v_new", _p), ("k_cache", _p), ("v_cache", _p),
+                ("block_table", _p), ("context_lens", _p),
+                ("B", _i), ("Hkv", _i), ("D", _i), ("block_size", _i),
+                ("max_blocks_per_seq", _i), ("num_blocks", _i)]
+
+
+class LinearArgs(ctypes.Structure):
+    _fields_ = [("x", _p), ("w", _p), ("y", _p), ("T", _i), ("K", _i), ("N", _i)]
+
+
 class AflexError(RuntimeError):
     def __init__(self, status: int, message: str):
         super().__init__(f"aflex status {status}: {message}")
@@ -74,6 +85,9 @@ def load():
         "aflex_moe_ffn": [FP, _p, ctypes.c_size_t, _p],
         "aflex_af_pipeline_workspace": [AP, FP, _i, I32P, _i, _SZ],
         "aflex_af_pipeline_step": [AP, FP, _i, I32P, _i, _p, ctypes.c_size_t, _p, _p],
+        "aflex_kv_append": [ctypes.POINTER(KvAppendArgs), _p],
+        "aflex_linear_workspace": [ctypes.POINTER(LinearArgs), _SZ],
+        "aflex_linear": [ctypes.POINTER(LinearArgs), _p, ctypes.c_size_t, _p],
     }
     for name, args in sig.items():
         fn = getattr(lib, name)
@@ -208,6 +222,32 @@ def moe_ffn(x, w, logits, k: int, y=None, routing: bool = False, stream=None, ws
     p, sz = _ws("moe", n.value, x.device, ws)
     _check(lib.aflex_moe_ffn(ctypes.byref(args), p, sz, _stream(stream)))
     return (y, r) if routing else y
+
+
+def kv_append(a, k_new, v_new, stream=None):
+    """Write each sequence's new token (position ctx-1) into a's paged pools, in place."""
+    lib = load()
+    args = KvAppendArgs(k_new=_ptr(k_new), v_new=_ptr(v_new), k_cache=_ptr(a.k_cache),
+                        v_cache=_ptr(a.v_cache), block_table=_ptr(a.block_table),
+                        context_lens=_ptr(a.context_lens), B=a.B, Hkv=a.Hkv, D=a.D,
+                        block_size=a.block_size, max_blocks_per_seq=a.max_blocks,
+                        num_blocks=a.num_blocks)
+    _check(lib.aflex_kv_append(ctypes.byref(args), _stream(stream)))
+
+
+def linear(x, w, y=None, stream=None, ws=None):
+    """y = x w^T (bf16), x [T, K], w [N, K]."""
+    lib = load()
+    T, K = x.shape
+    N = w.shape[0]
+    if y is None:
+        y = torch.empty(T, N, dtype=torch.bfloat16, device=x.device)
+    args = LinearArgs(x=_ptr(x), w=_ptr(w), y=_ptr(y), T=T, K=K, N=N)
+    n = ctypes.c_size_t()
+    _check(lib.aflex_linear_workspace(ctypes.byref(args), ctypes.byref(n)))
+    p, sz = _ws("linear", n.value, x.device, ws)
+    _check(lib.aflex_linear(ctypes.byref(args), p, sz, _stream(stream)))
+    return y
 
 
 _pipe_streams = {}

@@ -176,6 +176,46 @@ EventPool g_events;
 extern "C" {
 
 const char* aflex_last_error(void) { return g_err; }
+
+aflex_status aflex_kv_append(const aflex_kv_append_args* a, aflex_stream stream) {
+  REQUIRE(a, AFLEX_ERR_INVALID_ARG, "kv_append: args is NULL");
+  REQUIRE(a->k_new && a->v_new && a->k_cache && a->v_cache && a->block_table && a->context_lens,
+          AFLEX_ERR_INVALID_ARG, "kv_append: NULL tensor pointer");
+  REQUIRE(a->B >= 1 && a->Hkv >= 1 && a->num_blocks >= 1 && a->max_blocks_per_seq >= 1, AFLEX_ERR_INVALID_ARG,
+          "kv_append: B, Hkv, num_blocks, max_blocks_per_seq must be positive");
+  REQUIRE(a->D == 64 || a->D == 128, AFLEX_ERR_UNSUPPORTED, "kv_append: head_dim %d unsupported (64 or 128)", a->D);
+  REQUIRE(a->block_size == 16, AFLEX_ERR_UNSUPPORTED, "kv_append: block_size %d unsupported (16)", a->block_size);
+  REQUIRE(aligned16(a->k_new) && aligned16(a->v_new) && aligned16(a->k_cache) && aligned16(a->v_cache),
+          AFLEX_ERR_ALIGNMENT, "kv_append: tensors must be 16-byte aligned");
+  return hip_status(aflex::launch_kv_append(*a, (hipStream_t)stream), "kv_append");
+}
+
+static aflex_status check_linear(const aflex_linear_args* l) {
+  REQUIRE(l, AFLEX_ERR_INVALID_ARG, "linear: args is NULL");
+  REQUIRE(l->x && l->w && l->y, AFLEX_ERR_INVALID_ARG, "linear: NULL tensor pointer");
+  REQUIRE(l->T >= 1 && l->K >= 1 && l->N >= 1, AFLEX_ERR_INVALID_ARG, "linear: T, K, N must be positive");
+  REQUIRE(l->K % 64 == 0 && l->N % 64 == 0, AFLEX_ERR_UNSUPPORTED, "linear: K (%d) and N (%d) must be multiples of 64",
+          l->K, l->N);
+  REQUIRE(aligned16(l->x) && aligned16(l->w) && aligned16(l->y), AFLEX_ERR_ALIGNMENT,
+          "linear: tensors must be 16-byte aligned");
+  return AFLEX_OK;
+}
+
+aflex_status aflex_linear_workspace(const aflex_linear_args* l, size_t* bytes) {
+  REQUIRE(bytes, AFLEX_ERR_INVALID_ARG, "linear: bytes is NULL");
+  aflex_status s = check_linear(l);
+  if (s != AFLEX_OK) return s;
+  *bytes = aflex::linear_workspace_bytes(*l);
+  return AFLEX_OK;
+}
+
+aflex_status aflex_linear(const aflex_linear_args* l, void* ws, size_t ws_bytes, aflex_stream stream) {
+  aflex_status s = check_linear(l);
+  if (s != AFLEX_OK) return s;
+  s = check_ws(ws, ws_bytes, aflex::linear_workspace_bytes(*l), "linear");
+  if (s != AFLEX_OK) return s;
+  return hip_status(aflex::launch_linear(*l, ws, (hipStream_t)stream), "linear");
+}
 const char* aflex_version(void) { return "aflex 0.1 gfx950"; }
 
 aflex_status aflex_attn_decode_workspace(const aflex_attn_args* a, size_t* bytes) {

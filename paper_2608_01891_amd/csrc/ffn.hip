@@ -89,4 +89,41 @@ hipError_t launch_swiglu(const aflex_ffn_args& f, void* ws, hipStream_t stream) 
   return hipGetLastError();
 }
 
+// Linear layer y = x W^T: the down-GEMM tiles with split-K and the same
+// fixed-order reduction (bf16 out directly when a single split suffices).
+size_t linear_workspace_bytes(const aflex_linear_args& l) {
+  const FfnPlan pl = plan_dense(l.T, l.N, l.K);
+  return pl.down_splits > 1 ? align_up((size_t)pl.down_splits * l.T * l.N * 4, 256) : 256;
+}
+
+hipError_t launch_linear(const aflex_linear_args& l, void* ws, hipStream_t stream) {
+  const FfnPlan pl = plan_dense(l.T, l.N, l.K);
+  float* P = static_cast<float*>(ws);
+  GemmParams d = {};
+  d.A = l.x;
+  d.lda = l.K;
+  d.B0 = l.w;
+  d.ldb = l.K;
+  d.N = l.N;
+  d.K = l.K;
+  d.k_per_split = pl.down_kps;
+  d.splits = pl.down_splits;
+  d.M = l.T;
+  d.max_mtiles = (l.T + pl.bm - 1) / pl.bm;
+  d.n_ntiles = (l.N + down_bn(pl.bm) - 1) / down_bn(pl.bm);
+  d.mt_major = 0;
+  d.C = l.y;
+  d.ldc = l.N;
+  d.P = P;
+  d.p_split_stride = (long long)l.T * l.N;
+  d.ldp = l.N;
+  hipError_t e = launch_down(pl.bm, pl.down_splits > 1, d, stream);
+  if (e != hipSuccess || pl.down_splits == 1) return e;
+  const long long n4 = (long long)l.T * l.N / 4;
+  ProfScope ps("splitk_reduce", stream);
+  splitk_reduce_kernel<<<(unsigned)((n4 + 255) / 256), 256, 0, stream>>>(P, d.p_split_stride, pl.down_splits, n4,
+                                                                       l.y);
+  return hipGetLastError();
+}
+
 }  // namespace aflex

@@ -68,7 +68,15 @@ __device__ __forceinline__ uint32_t lds_offset(const void* p) {
 // callers order it with explicit s_waitcnt vmcnt and barriers.
 __device__ __forceinline__ void lds_dma16(const void* gptr, uint32_t lds) {
   const uint32_t lds_s = __builtin_amdgcn_readfirstlane(lds);  // uniform across the wave
-  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(gptr), "s"(lds_s) : "memory", "m0");
+  uint32_t saved;  // m0 is reserved to the compiler: restore it after the load
+  asm volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %2\n\t"
+      "global_load_lds_dwordx4 %1, off\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "v"(gptr), "s"(lds_s)
+      : "memory");
 }
 
 __device__ __forceinline__ int xcd_remap(int w, int nwg) {
