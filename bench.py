@@ -382,6 +382,21 @@ def main():
                 "hbm_frac": round(byts / (ms * 1e-3) / PEAK_HBM, 4),
                 "tok_per_s": round(T / (ms * 1e-3), 1),
                 "kernels": {kname: round(v[1] / v[0], 5) for kname, v in kp.items()}}
+            if T == 256:
+                # the whole MoE FFN block: RMSNorm, router GEMM, experts, residual
+                gamma = (1.0 + 0.1 * synth.normal_tensor(seed, 50, (H,), dtype=torch.float32,
+                                                         device=dev)).to(torch.bfloat16)
+                wr = synth.normal_tensor(seed, 51, (8, H), scale=0.02, device=dev)
+                aflex.moe_block(wm.x, wm.ffn, gamma, wr, 2, residual=True, y=yT)
+                aflex.profile_start(["rmsnorm_router"])
+                ms_b = timed(lambda: aflex.moe_block(wm.x, wm.ffn, gamma, wr, 2, residual=True,
+                                                     y=yT), 10)
+                kp = aflex.profile_stop()
+                ops["moe_block_mixtral_T256"] = {
+                    "ms": round(ms_b, 5), "GB_per_s": round(byts / (ms_b * 1e-3) / 1e9, 1),
+                    "hbm_frac": round(byts / (ms_b * 1e-3) / PEAK_HBM, 4),
+                    "tok_per_s": round(T / (ms_b * 1e-3), 1),
+                    "kernels": {kname: round(v[1] / v[0], 5) for kname, v in kp.items()}}
             del wm
         result["operators"] = ops
 

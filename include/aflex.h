@@ -120,6 +120,27 @@ aflex_status aflex_moe_ffn_workspace(const aflex_ffn_args *f, size_t *bytes);
 aflex_status aflex_moe_ffn(const aflex_ffn_args *f, void *workspace, size_t workspace_bytes,
                            aflex_stream stream);
 
+/* MoE FFN block of a Mixtral layer: the normalisation and router that come   */
+/* before the experts (section 6.1 names the model):                         */
+/*   xn     = x / sqrt(mean(x^2) + eps) * norm_weight        (per token)     */
+/*   logits = xn W_r^T  (fp32, from the unrounded xn)        W_r = [E, H]    */
+/*   y      = MoE(bf16(xn), logits)  (+ x when residual != 0)                */
+/* ffn.x is the block input; ffn.router_logits is ignored (computed); the    */
+/* optional MoE outputs of ffn are written as by aflex_moe_ffn.              */
+typedef struct aflex_moe_block_args {
+  aflex_ffn_args ffn;              /* MoE weights and shapes, ffn.x = input [T, H] */
+  const aflex_bf16 *norm_weight;   /* [H] RMSNorm gain */
+  const aflex_bf16 *router_weight; /* [E, H] */
+  float eps;                       /* RMSNorm epsilon (>= 0) */
+  int32_t residual;                /* nonzero: add x to the output */
+  float *router_logits_out;        /* optional [T, E] fp32 output (NULL: not written) */
+} aflex_moe_block_args;
+
+/* Supported: as aflex_moe_ffn, and H <= 16384. */
+aflex_status aflex_moe_block_workspace(const aflex_moe_block_args *m, size_t *bytes);
+aflex_status aflex_moe_block(const aflex_moe_block_args *m, void *workspace, size_t workspace_bytes,
+                             aflex_stream stream);
+
 /* ------------------------------------------------------------------------ */
 /* Interleaved A/F layer step (section 4.3, "Interleaved A/F Pipeline"; Eq. 2)*/
 /* The batch is cut into M contiguous microbatches of host-known sizes        */
@@ -189,7 +210,7 @@ aflex_status aflex_linear(const aflex_linear_args *l, void *workspace, size_t wo
 /* name is in the comma-separated list `kernels` (NULL or "" = all) is        */
 /* bracketed by two HIP events on the stream it is launched on. Kernel names: */
 /* attn_split, attn_merge, gemm_gate_up, gemm_down, splitk_reduce, moe_route, */
-/* moe_combine, kv_append. aflex_profile_stop waits for those events and writes one line */
+/* moe_combine, kv_append, rmsnorm_router. aflex_profile_stop waits for those events and writes one line */
 /* per kernel into `report` (host buffer of `len` bytes, truncated to fit):   */
 /*   "<name> <launches> <total_ms> <min_ms> <max_ms>
 "                      */

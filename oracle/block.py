@@ -9,10 +9,16 @@ section 1 and section 2), and the attention output is projected back to the
 hidden size before it crosses the A/F boundary (section 4.3: the attention
 group sends its output to the FFN group).
 
+The FFN stage of the MoE model starts the same way on the F side: the
+Mixtral layer normalises the hidden state (RMSNorm) and computes the router
+logits before the experts run (section 6.1 names the model):
+
     kv_append:  j = ctx_b - 1 (the new token is the last cached one)
                 K[table[b, j // bs], g, j % bs, :] = k_new[b, g, :]
                 V[table[b, j // bs], g, :, j % bs] = v_new[b, g, :]
     linear:     y = x W^T   (W in [out_features, in_features])
+    rmsnorm:    x / sqrt(mean(x^2) + eps) * gamma
+    moe_block:  y = MoE(RMSNorm(x), RMSNorm(x) W_r^T) (+ x with the residual)
 
 Readings: context_lens already counts the new token; sequences
 with ctx_b = 0 append nothing; the projection has no bias.
@@ -20,6 +26,8 @@ with ctx_b = 0 append nothing; the projection has no bias.
 from __future__ import annotations
 
 import torch
+
+from .moe import moe_ffn
 
 
 def kv_append(k_cache, v_cache, block_table, context_lens, k_new, v_new):
@@ -41,3 +49,28 @@ def kv_append(k_cache, v_cache, block_table, context_lens, k_new, v_new):
 def linear(x, w):
     """y [T, N] float64 for x [T, K], w [N, K]."""
     return x.to(torch.float64) @ w.to(torch.float64).T
+
+
+def rmsnorm(x, gamma, eps: float):
+    """x / sqrt(mean(x^2) + eps) * gamma over the last dimension (float64)."""
+    x = x.to(torch.float64)
+    inv = 1.0 / torch.sqrt((x * x).mean(dim=-1, keepdim=True) + eps)
+    return x * inv * gamma.to(torch.float64)
+
+
+def moe_block(x, gamma, eps: float, w_router, w_gate, w_up, w_down, k: int, residual: bool,
+              token_indices=None):
+    """The MoE FFN block of a Mixtral layer: normalise, route, mix experts.
+
+        xn     = RMSNorm(x)
+        logits = xn W_r^T                       (W_r [E, H])
+        y      = MoE(xn, logits) (+ x if residual)
+
+    Returns y [T, H], logits [T, E], ids [T, k] (float64 / int64).
+    """
+    xn = rmsnorm(x, gamma, eps)
+    logits = xn @ w_router.to(torch.float64).T
+    y, ids, _ = moe_ffn(xn, logits, w_gate, w_up, w_down, k, token_indices=token_indices)
+    if residual:
+        y = y + x.to(torch.float64)
+    return y, logits, ids

@@ -49,6 +49,11 @@ class LinearArgs(ctypes.Structure):
     _fields_ = [("x", _p), ("w", _p), ("y", _p), ("T", _i), ("K", _i), ("N", _i)]
 
 
+class MoeBlockArgs(ctypes.Structure):
+    _fields_ = [("ffn", FfnArgs), ("norm_weight", _p), ("router_weight", _p),
+                ("eps", ctypes.c_float), ("residual", _i), ("router_logits_out", _p)]
+
+
 class AflexError(RuntimeError):
     def __init__(self, status: int, message: str):
         super().__init__(f"aflex status {status}: {message}")
@@ -86,6 +91,8 @@ def load():
         "aflex_af_pipeline_workspace": [AP, FP, _i, I32P, _i, _SZ],
         "aflex_af_pipeline_step": [AP, FP, _i, I32P, _i, _p, ctypes.c_size_t, _p, _p],
         "aflex_kv_append": [ctypes.POINTER(KvAppendArgs), _p],
+        "aflex_moe_block_workspace": [ctypes.POINTER(MoeBlockArgs), _SZ],
+        "aflex_moe_block": [ctypes.POINTER(MoeBlockArgs), _p, ctypes.c_size_t, _p],
         "aflex_linear_workspace": [ctypes.POINTER(LinearArgs), _SZ],
         "aflex_linear": [ctypes.POINTER(LinearArgs), _p, ctypes.c_size_t, _p],
     }
@@ -248,6 +255,33 @@ def linear(x, w, y=None, stream=None, ws=None):
     p, sz = _ws("linear", n.value, x.device, ws)
     _check(lib.aflex_linear(ctypes.byref(args), p, sz, _stream(stream)))
     return y
+
+
+def moe_block(x, w, norm_weight, router_weight, k: int, eps: float = 1e-5, residual: bool = False,
+              y=None, routing: bool = False, stream=None, ws=None):
+    """y = MoE(RMSNorm(x)) (+ x): normalisation, router GEMM and experts on the device.
+
+    With routing=True also returns the router logits and the routing outputs."""
+    lib = load()
+    T = x.shape[0]
+    if y is None:
+        y = torch.empty(T, w.H, dtype=torch.bfloat16, device=x.device)
+    r = None
+    logits = None
+    if routing:
+        r = {"topk_ids": torch.empty(T, k, dtype=torch.int32, device=x.device),
+             "topk_w": torch.empty(T, k, dtype=torch.float32, device=x.device),
+             "expert_offsets": torch.empty(w.E + 1, dtype=torch.int32, device=x.device),
+             "sorted_pairs": torch.empty(T * k, dtype=torch.int32, device=x.device)}
+        logits = torch.empty(T, w.E, dtype=torch.float32, device=x.device)
+    args = MoeBlockArgs(ffn=ffn_args(x, w, y, None, k, r), norm_weight=_ptr(norm_weight),
+                        router_weight=_ptr(router_weight), eps=eps, residual=int(residual),
+                        router_logits_out=_ptr(logits))
+    n = ctypes.c_size_t()
+    _check(lib.aflex_moe_block_workspace(ctypes.byref(args), ctypes.byref(n)))
+    p, sz = _ws("moe_block", n.value, x.device, ws)
+    _check(lib.aflex_moe_block(ctypes.byref(args), p, sz, _stream(stream)))
+    return (y, logits, r) if routing else y
 
 
 _pipe_streams = {}

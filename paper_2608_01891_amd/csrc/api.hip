@@ -266,6 +266,36 @@ aflex_status aflex_moe_ffn(const aflex_ffn_args* f, void* ws, size_t ws_bytes, a
   return hip_status(aflex::launch_moe(*f, ws, (hipStream_t)stream), "moe");
 }
 
+static aflex_status check_moe_block(const aflex_moe_block_args* m) {
+  REQUIRE(m, AFLEX_ERR_INVALID_ARG, "moe_block: args is NULL");
+  REQUIRE(m->norm_weight && m->router_weight, AFLEX_ERR_INVALID_ARG, "moe_block: NULL norm or router weight");
+  REQUIRE(isfinite(m->eps) && m->eps >= 0.f, AFLEX_ERR_INVALID_ARG, "moe_block: eps must be finite and >= 0");
+  aflex_ffn_args f = m->ffn;
+  f.router_logits = reinterpret_cast<const float*>(m->router_weight);  // computed: only non-NULL matters
+  aflex_status s = check_ffn(&f, true, true);
+  if (s != AFLEX_OK) return s;
+  REQUIRE(f.H <= 16384, AFLEX_ERR_UNSUPPORTED, "moe_block: H=%d above 16384", f.H);
+  REQUIRE(aligned16(m->norm_weight) && aligned16(m->router_weight), AFLEX_ERR_ALIGNMENT,
+          "moe_block: weights must be 16-byte aligned");
+  return AFLEX_OK;
+}
+
+aflex_status aflex_moe_block_workspace(const aflex_moe_block_args* m, size_t* bytes) {
+  REQUIRE(bytes, AFLEX_ERR_INVALID_ARG, "moe_block: bytes is NULL");
+  aflex_status s = check_moe_block(m);
+  if (s != AFLEX_OK) return s;
+  *bytes = aflex::moe_block_workspace_bytes(*m);
+  return AFLEX_OK;
+}
+
+aflex_status aflex_moe_block(const aflex_moe_block_args* m, void* ws, size_t ws_bytes, aflex_stream stream) {
+  aflex_status s = check_moe_block(m);
+  if (s != AFLEX_OK) return s;
+  s = check_ws(ws, ws_bytes, aflex::moe_block_workspace_bytes(*m), "moe_block");
+  if (s != AFLEX_OK) return s;
+  return hip_status(aflex::launch_moe_block(*m, ws, (hipStream_t)stream), "moe_block");
+}
+
 aflex_status aflex_af_pipeline_workspace(const aflex_attn_args* a, const aflex_ffn_args* f, int32_t M,
                                          const int32_t* mb, int32_t L, size_t* bytes) {
   REQUIRE(bytes, AFLEX_ERR_INVALID_ARG, "pipeline: bytes is NULL");

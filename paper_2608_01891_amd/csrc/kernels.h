@@ -25,12 +25,19 @@ hipError_t launch_linear(const aflex_linear_args& l, void* ws, hipStream_t strea
 
 // Top-k MoE FFN (moe.hip).
 size_t moe_workspace_bytes(const aflex_ffn_args& f);
-hipError_t launch_moe(const aflex_ffn_args& f, void* ws, hipStream_t stream);
+// residual (optional, [T, H]) is added to the output in the combine step.
+hipError_t launch_moe(const aflex_ffn_args& f, void* ws, hipStream_t stream, const uint16_t* residual = nullptr);
 // The two halves of launch_moe: routing (depends only on the logits) and the
 // expert computation, with separate workspace blocks.
 size_t moe_route_bytes(const aflex_ffn_args& f);
 size_t moe_expert_bytes(const aflex_ffn_args& f);
 hipError_t launch_moe_route(const aflex_ffn_args& f, void* route_ws, hipStream_t stream);
-hipError_t launch_moe_experts(const aflex_ffn_args& f, void* route_ws, void* expert_ws, hipStream_t stream);
+hipError_t launch_moe_experts(const aflex_ffn_args& f, void* route_ws, void* expert_ws, hipStream_t stream,
+                              const uint16_t* residual = nullptr);
+
+// RMSNorm + router + MoE block (moe_block.hip).
+constexpr int kMaxRouterE = 64;
+size_t moe_block_workspace_bytes(const aflex_moe_block_args& m);
+hipError_t launch_moe_block(const aflex_moe_block_args& m, void* ws, hipStream_t stream);
 
 }  // namespace aflex

@@ -186,6 +186,7 @@ __global__ __launch_bounds__(256) void moe_route_kernel(const float* __restrict_
 __global__ __launch_bounds__(256) void moe_combine_kernel(const float* __restrict__ P, long long split_stride,
                                                           int splits, const int32_t* __restrict__ pos,
                                                           const float* __restrict__ w, int k, int H,
+                                                          const uint16_t* __restrict__ residual,
                                                           uint16_t* __restrict__ y) {
   const int t = blockIdx.x;
   const int c = (blockIdx.y * 256 + threadIdx.x) * 4;
@@ -197,6 +198,13 @@ __global__ __launch_bounds__(256) void moe_combine_kernel(const float* __restric
     f32x4 s = *reinterpret_cast<const f32x4*>(P + row * H + c);
     for (int sp = 1; sp < splits; ++sp) s += *reinterpret_cast<const f32x4*>(P + sp * split_stride + row * H + c);
     acc += wt * s;
+  }
+  if (residual) {
+    const ushort4 rv = *reinterpret_cast<const ushort4*>(residual + (size_t)t * H + c);
+    acc[0] += bf2f(rv.x);
+    acc[1] += bf2f(rv.y);
+    acc[2] += bf2f(rv.z);
+    acc[3] += bf2f(rv.w);
   }
   ushort4 o;
   o.x = f2bf(acc[0]);
@@ -219,14 +227,15 @@ hipError_t launch_moe_route(const aflex_ffn_args& f, void* route_ws, hipStream_t
   return hipGetLastError();
 }
 
-hipError_t launch_moe(const aflex_ffn_args& f, void* ws, hipStream_t stream) {
+hipError_t launch_moe(const aflex_ffn_args& f, void* ws, hipStream_t stream, const uint16_t* residual) {
   const MoeLayout L = moe_layout(f);
   hipError_t e = launch_moe_route(f, ws, stream);
   if (e != hipSuccess) return e;
-  return launch_moe_experts(f, ws, static_cast<char*>(ws) + L.route_total, stream);
+  return launch_moe_experts(f, ws, static_cast<char*>(ws) + L.route_total, stream, residual);
 }
 
-hipError_t launch_moe_experts(const aflex_ffn_args& f, void* route_ws, void* expert_ws, hipStream_t stream) {
+hipError_t launch_moe_experts(const aflex_ffn_args& f, void* route_ws, void* expert_ws, hipStream_t stream,
+                              const uint16_t* residual) {
   const MoeLayout L = moe_layout(f);
   char* w = static_cast<char*>(route_ws);
   char* xw = static_cast<char*>(expert_ws);
@@ -286,7 +295,8 @@ hipError_t launch_moe_experts(const aflex_ffn_args& f, void* route_ws, void* exp
 
   dim3 grid(f.T, (f.H / 4 + 255) / 256);
   ProfScope ps("moe_combine", stream);
-  moe_combine_kernel<<<grid, 256, 0, stream>>>(P, d.p_split_stride, L.down_splits, pos, wts, f.k, f.H, f.y);
+  moe_combine_kernel<<<grid, 256, 0, stream>>>(P, d.p_split_stride, L.down_splits, pos, wts, f.k, f.H, residual,
+                                               f.y);
   return hipGetLastError();
 }
 

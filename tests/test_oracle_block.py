@@ -60,3 +60,37 @@ def test_linear_bruteforce_and_identity():
             assert abs(float(y[t, n]) - sum(float(x[t, kk]) * float(w[n, kk]) for kk in range(5))) < 1e-12
     assert torch.equal(oracle.linear(x, torch.eye(5, dtype=torch.float64)), x)
     assert y.shape == (3, 4)  # [T, out_features]: catches a transposed weight
+
+
+def test_rmsnorm_bruteforce_and_invariants():
+    rng = np.random.default_rng(94)
+    x = torch.from_numpy(rng.standard_normal((3, 6)))
+    g = torch.from_numpy(rng.standard_normal(6))
+    y = oracle.rmsnorm(x, g, 1e-5)
+    for t in range(3):
+        ms = sum(float(v) ** 2 for v in x[t]) / 6
+        for i in range(6):
+            assert abs(float(y[t, i]) - float(x[t, i]) / math.sqrt(ms + 1e-5) * float(g[i])) < 1e-12
+    # scale invariance without eps; a constant row maps to gamma (unit gain) times its sign
+    assert torch.allclose(oracle.rmsnorm(5.0 * x, g, 0.0), oracle.rmsnorm(x, g, 0.0), rtol=1e-13)
+    c = torch.full((1, 6), -3.0, dtype=torch.float64)
+    assert torch.allclose(oracle.rmsnorm(c, torch.ones(6, dtype=torch.float64), 0.0),
+                          -torch.ones(1, 6, dtype=torch.float64))
+
+
+def test_moe_block_routes_on_normalised_coordinates_and_adds_residual():
+    # one-hot router rows: logit e is coordinate e of the normalised input
+    x, w, _ = synth.custom_ffn(95, 5, 64, 64, E=4)
+    gamma = torch.ones(64, dtype=torch.bfloat16)
+    wr = torch.zeros(4, 64, dtype=torch.float64)
+    for e in range(4):
+        wr[e, e] = 1.0
+    y, logits, ids = oracle.moe_block(x, gamma, 1e-6, wr, w.w_gate, w.w_up, w.w_down, 2, False)
+    xn = oracle.rmsnorm(x, gamma, 1e-6)
+    assert torch.equal(logits, xn[:, :4])
+    ref_ids = np.argsort(-xn[:, :4].numpy(), axis=1, kind="stable")[:, :2]
+    assert np.array_equal(ids.numpy(), ref_ids)
+    y2, _, _ = oracle.moe_block(x, gamma, 1e-6, wr, w.w_gate, w.w_up, w.w_down, 2, True)
+    assert torch.allclose(y2 - y, x.double(), rtol=0, atol=1e-15)
+    ref, _, _ = oracle.moe_ffn(xn, xn[:, :4], w.w_gate, w.w_up, w.w_down, 2)
+    assert torch.equal(y, ref)
