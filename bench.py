@@ -276,6 +276,44 @@ def main():
         variants["eq2_ms"] = {"M=1": round(plan.eq2_layer_time(t_a, t_f, 0.0, 1), 4),
                               "M=4": round(plan.eq2_layer_time(t_a, t_f, 0.0, 4), 4)}
         variants["byte_roofline_ms"] = round(step_bytes / PEAK_HBM * 1e3, 4)
+        # dynamic microbatch depth + adaptive request batching: Eq. 2 over the
+        # stage curves profiled here, and the measured layer time of each split
+        prof_a, prof_f = {}, {}
+
+        def stage_times(n):
+            if n not in prof_a:
+                am = synth.AttnInputs(q=a.q[:n], k_cache=a.k_cache, v_cache=a.v_cache,
+                                      block_table=a.block_table[:n], context_lens=a.context_lens[:n],
+                                      B=n, Hq=a.Hq, Hkv=a.Hkv, D=a.D, block_size=16,
+                                      max_blocks=a.max_blocks, num_blocks=a.num_blocks,
+                                      max_context_len=a.max_context_len)
+                o = torch.empty(n, a.Hq, a.D, dtype=torch.bfloat16, device=dev)
+                aflex.attn_decode(am, out=o)
+                prof_a[n] = timed(lambda: aflex.attn_decode(am, out=o), 3)
+                yv = torch.empty(n, H, dtype=torch.bfloat16, device=dev)
+                aflex.moe_ffn(o.view(n, H), f, logits[:n], k, y=yv)
+                prof_f[n] = timed(lambda: aflex.moe_ffn(o.view(n, H), f, logits[:n], k, y=yv), 3)
+            return prof_a[n], prof_f[n]
+
+        def measured(m):
+            step(m)
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            for _ in range(5):
+                step(m)
+            torch.cuda.synchronize()
+            return (time.perf_counter() - t0) * 1e3 / 5
+        cands = plan.candidate_splits(B)
+        eq2_best, eq2_ms = plan.choose_split(
+            cands, lambda m: plan.eq2_predict(m, lambda n: stage_times(n)[0], lambda n: stage_times(n)[1]))
+        meas = {tuple(m): measured(m) for m in cands}
+        best = min(meas, key=meas.get)
+        variants["planner"] = {
+            "candidates_ms": {"+".join(map(str, m)): round(v, 4) for m, v in meas.items()},
+            "eq2_choice": "+".join(map(str, eq2_best)), "eq2_predicted_ms": round(eq2_ms, 4),
+            "eq2_choice_measured_ms": round(meas[tuple(eq2_best)], 4),
+            "measured_choice": "+".join(map(str, best)), "measured_ms": round(meas[best], 4),
+            "measured_tok_per_s": round(B / (meas[best] * 1e-3), 1)}
         variants["t_F_over_t_A"] = round(t_f / t_a, 3)
         ops["af_pipeline"] = variants
 
