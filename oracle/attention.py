@@ -14,7 +14,7 @@ The definition used for one decode token of sequence b and query head h:
     p_j    = exp(s_j - max s) / sum_j' exp(s_j' - max s)
     out    = sum_j p_j v_j
 
-Readings where the paper is silent (all listed in the design doc):
+Readings taken where the paper is silent:
   * K pool layout [num_blocks, Hkv, bs, D]; V pool layout [num_blocks, Hkv, D, bs]
     (the token index is fastest in V). The layout is part of the interface.
   * ctx_b counts the valid cached tokens (the new token's K/V already appended);

@@ -20,7 +20,7 @@ logits before the experts run (section 6.1 names the model):
     rmsnorm:    x / sqrt(mean(x^2) + eps) * gamma
     moe_block:  y = MoE(RMSNorm(x), RMSNorm(x) W_r^T) (+ x with the residual)
 
-Readings: context_lens already counts the new token; sequences
+Readings taken where the paper is silent: context_lens already counts the new token; sequences
 with ctx_b = 0 append nothing; the projection has no bias.
 """
 from __future__ import annotations

@@ -16,7 +16,7 @@ Routing tables (the index work of the permute/un-permute steps):
     sorted      = pair ids t*k+j ordered by (expert, token, slot)
     position    = inverse of sorted: position[t*k+j] = rank of that pair
 
-Readings (the design doc lists them): logits are fp32 and widened exactly, so the
+Readings taken where the paper is silent: logits are fp32 and widened exactly, so the
 ordering is the fp32 ordering; ties go to the lower expert id; the weights are
 the softmax over the selected logits, which equals the full softmax
 renormalised over the top-k.

@@ -13,7 +13,7 @@ running, for every microbatch i and layer l in order,
                                              microbatch i's router logits)
     q_i = y viewed as [n_i, Hq, D]          (input of the next layer step)
 
-Readings: the attention output feeds the FFN directly (no output
+Readings taken where the paper is silent: the attention output feeds the FFN directly (no output
 projection or normalisation, which lie outside the operator pair); later layer
 steps reuse the same KV cache and weights; microbatches are contiguous slices
 of the batch in order.
