@@ -27,3 +27,4 @@ from .ffn import silu, swiglu_ffn  # noqa: F401
 from .moe import route_topk, routing_tables, moe_ffn  # noqa: F401
 from .pipeline import af_layer_steps  # noqa: F401
 from .block import kv_append, linear, moe_block, rmsnorm  # noqa: F401
+from .prefill import attention_prefill  # noqa: F401

@@ -118,7 +118,8 @@ def normal_tensor(seed: int, stream: int, shape, scale: float = 1.0,
 
 
 # stream ids of the bulk tensors
-STREAM = {"q": 1, "k": 2, "v": 3, "x": 4, "w_gate": 5, "w_up": 6, "w_down": 7}
+STREAM = {"q": 1, "k": 2, "v": 3, "x": 4, "w_gate": 5, "w_up": 6, "w_down": 7,
+          "prefill_q": 8, "prefill_k": 9, "prefill_v": 10}
 WEIGHT_SIGMA = 0.02
 BLOCK_SIZE = 16
 
@@ -278,6 +279,56 @@ def af_pipeline(device="cpu", M: int = 4) -> Workload:
     return Workload(f"af-pipeline-B256-M{M}", seed, attn=attn, ffn=ffn,
                     router_logits=torch.from_numpy(logits).to(device), top_k=2,
                     microbatches=mbs)
+
+
+@dataclass
+class PrefillInputs:
+    q: torch.Tensor           # [T, Hq, D] bf16, prompts packed back to back
+    k: torch.Tensor           # [T, Hkv, D] bf16
+    v: torch.Tensor           # [T, Hkv, D] bf16
+    cu_seqlens: torch.Tensor  # [B + 1] int32, prompt b is tokens cu[b] .. cu[b+1] - 1
+    lens: list
+    Hq: int
+    Hkv: int
+    D: int
+
+    @property
+    def T(self) -> int:
+        return int(sum(self.lens))
+
+    @property
+    def max_seqlen(self) -> int:
+        return max(max(self.lens), 0)
+
+    def to(self, device):
+        d = dict(self.__dict__)
+        for k in ("q", "k", "v", "cu_seqlens"):
+            d[k] = d[k].to(device)
+        return PrefillInputs(**d)
+
+
+def make_prefill(seed: int, lens, Hq: int, Hkv: int, D: int, device="cpu") -> PrefillInputs:
+    """Packed prompts of the given lengths; q, k, v are standard normal bf16."""
+    lens = [int(n) for n in lens]
+    cu = np.concatenate([[0], np.cumsum(lens, dtype=np.int64)]).astype(np.int32)
+    T = int(cu[-1])
+    q = normal_tensor(seed, STREAM["prefill_q"], (T, Hq, D), device=device)
+    k = normal_tensor(seed, STREAM["prefill_k"], (T, Hkv, D), device=device)
+    v = normal_tensor(seed, STREAM["prefill_v"], (T, Hkv, D), device=device)
+    return PrefillInputs(q=q, k=k, v=v, cu_seqlens=torch.from_numpy(cu).to(device),
+                         lens=lens, Hq=Hq, Hkv=Hkv, D=D)
+
+
+# Prefill workloads at the paper's two prompt lengths (section 6.1: 128- and
+# 4096-token inputs), with the attention shapes of the two models.
+PREFILL_SHAPES = {"qwen3-32b": (64, 8, 128), "mixtral-8x7b": (32, 8, 128)}
+
+
+def prefill_workload(model: str = "qwen3-32b", prompt_len: int = 4096, prompts: int = 2,
+                     device="cpu") -> PrefillInputs:
+    Hq, Hkv, D = PREFILL_SHAPES[model]
+    seed = 5 if prompt_len >= 1024 else 6
+    return make_prefill(seed, [prompt_len] * prompts, Hq, Hkv, D, device=device)
 
 
 def custom_attention(seed: int, B: int, Hq: int, Hkv: int, D: int, ctx, ctx_hi: int | None = None,
