@@ -14,6 +14,7 @@
  *   aflex_ffn_swiglu        dense SwiGLU FFN (Qwen3-32B-shaped layers)
  *   aflex_moe_ffn           top-k mixture-of-experts SwiGLU FFN (Mixtral-8x7B)
  *   aflex_af_pipeline_step  M microbatches of A then F on two HIP streams
+ *   aflex_attn_prefill      causal attention over packed prompts (prefill)
  *
  * Conventions shared by every entry point
  *  - bf16 tensors are passed as raw bit patterns (aflex_bf16 = uint16_t).
@@ -203,6 +204,32 @@ aflex_status aflex_linear_workspace(const aflex_linear_args *l, size_t *bytes);
 aflex_status aflex_linear(const aflex_linear_args *l, void *workspace, size_t workspace_bytes,
                           aflex_stream stream);
 
+/* Causal prefill attention (section 2, "LLM Serving": prefill processes the  */
+/* prompt tokens in parallel; section 3.2 profiles prefill Attention, PA,     */
+/* next to decode). Prompts are packed back to back: prompt b is tokens       */
+/* cu_seqlens[b] .. cu_seqlens[b+1]-1 of q, k, v. For token i of prompt b and */
+/* query head h (g = h / (Hq/Hkv)):                                           */
+/*   out[cu_b+i, h] = sum_{j<=i} softmax_j(scale <q[cu_b+i,h], k[cu_b+j,g]>)  */
+/*                    v[cu_b+j, g]                                            */
+/* bf16 in, fp32 accumulation, bf16 out (round to nearest even).              */
+typedef struct aflex_prefill_args {
+  const aflex_bf16 *q;          /* [T, Hq, D] */
+  const aflex_bf16 *k;          /* [T, Hkv, D] */
+  const aflex_bf16 *v;          /* [T, Hkv, D] */
+  const int32_t *cu_seqlens;    /* [B+1] device, 0 = cu[0] <= cu[1] <= ... <= cu[B] = T */
+  aflex_bf16 *out;              /* [T, Hq, D] */
+  int32_t B, T, Hq, Hkv, D;
+  int32_t max_seqlen;           /* host-known bound on every prompt length; sizes the grid */
+  float scale;                  /* softmax scale; 0 selects 1/sqrt(D) */
+} aflex_prefill_args;
+
+/* Supported: D == 128, Hq % Hkv == 0, B <= 65535. No workspace.               */
+/* cu_seqlens lives in device memory and is not checked on the host: the      */
+/* kernel clamps each prompt to [0, T], so a bad array cannot make it read or */
+/* write outside q, k, v, out; rows of a prompt longer than max_seqlen past   */
+/* position max_seqlen are not written. Empty prompts produce no rows.        */
+aflex_status aflex_attn_prefill(const aflex_prefill_args *a, aflex_stream stream);
+
 /* ------------------------------------------------------------------------ */
 /* Per-kernel timing, the single-GPU analogue of the paper's per-operator     */
 /* latency profiling (section 4.1; section 5, "Profiling module"). Between    */
@@ -210,10 +237,10 @@ aflex_status aflex_linear(const aflex_linear_args *l, void *workspace, size_t wo
 /* name is in the comma-separated list `kernels` (NULL or "" = all) is        */
 /* bracketed by two HIP events on the stream it is launched on. Kernel names: */
 /* attn_split, attn_merge, gemm_gate_up, gemm_down, splitk_reduce, moe_route, */
-/* moe_combine, kv_append, rmsnorm_router. aflex_profile_stop waits for those events and writes one line */
-/* per kernel into `report` (host buffer of `len` bytes, truncated to fit):   */
-/*   "<name> <launches> <total_ms> <min_ms> <max_ms>
-"                      */
+/* moe_combine, kv_append, rmsnorm_router, attn_prefill. aflex_profile_stop */
+/* waits for those events and writes one line per kernel into `report`      */
+/* (host buffer of `len` bytes, truncated to fit):                           */
+/*   <name> <launches> <total_ms> <min_ms> <max_ms>                          */
 /* Off by default; while off no event is recorded.                            */
 /* ------------------------------------------------------------------------ */
 aflex_status aflex_profile_start(const char *kernels);

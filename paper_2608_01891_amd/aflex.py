@@ -54,6 +54,12 @@ class MoeBlockArgs(ctypes.Structure):
                 ("eps", ctypes.c_float), ("residual", _i), ("router_logits_out", _p)]
 
 
+class PrefillArgs(ctypes.Structure):
+    _fields_ = [("q", _p), ("k", _p), ("v", _p), ("cu_seqlens", _p), ("out", _p),
+                ("B", _i), ("T", _i), ("Hq", _i), ("Hkv", _i), ("D", _i),
+                ("max_seqlen", _i), ("scale", ctypes.c_float)]
+
+
 class AflexError(RuntimeError):
     def __init__(self, status: int, message: str):
         super().__init__(f"aflex status {status}: {message}")
@@ -95,6 +101,7 @@ def load():
         "aflex_moe_block": [ctypes.POINTER(MoeBlockArgs), _p, ctypes.c_size_t, _p],
         "aflex_linear_workspace": [ctypes.POINTER(LinearArgs), _SZ],
         "aflex_linear": [ctypes.POINTER(LinearArgs), _p, ctypes.c_size_t, _p],
+        "aflex_attn_prefill": [ctypes.POINTER(PrefillArgs), _p],
     }
     for name, args in sig.items():
         fn = getattr(lib, name)
@@ -240,6 +247,19 @@ def kv_append(a, k_new, v_new, stream=None):
                         block_size=a.block_size, max_blocks_per_seq=a.max_blocks,
                         num_blocks=a.num_blocks)
     _check(lib.aflex_kv_append(ctypes.byref(args), _stream(stream)))
+
+
+def attn_prefill(p, out=None, max_seqlen=None, scale: float = 0.0, stream=None):
+    """Causal attention over the packed prompts of ``p`` (synth.PrefillInputs on the device)."""
+    lib = load()
+    T, Hq, D = p.q.shape
+    if out is None:
+        out = torch.empty(T, Hq, D, dtype=torch.bfloat16, device=p.q.device)
+    args = PrefillArgs(q=_ptr(p.q), k=_ptr(p.k), v=_ptr(p.v), cu_seqlens=_ptr(p.cu_seqlens),
+                       out=_ptr(out), B=p.cu_seqlens.numel() - 1, T=T, Hq=Hq, Hkv=p.k.shape[1], D=D,
+                       max_seqlen=p.max_seqlen if max_seqlen is None else max_seqlen, scale=scale)
+    _check(lib.aflex_attn_prefill(ctypes.byref(args), _stream(stream)))
+    return out
 
 
 def linear(x, w, y=None, stream=None, ws=None):

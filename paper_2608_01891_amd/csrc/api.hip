@@ -190,6 +190,23 @@ aflex_status aflex_kv_append(const aflex_kv_append_args* a, aflex_stream stream)
   return hip_status(aflex::launch_kv_append(*a, (hipStream_t)stream), "kv_append");
 }
 
+aflex_status aflex_attn_prefill(const aflex_prefill_args* a, aflex_stream stream) {
+  REQUIRE(a, AFLEX_ERR_INVALID_ARG, "prefill: args is NULL");
+  REQUIRE(a->q && a->k && a->v && a->cu_seqlens && a->out, AFLEX_ERR_INVALID_ARG, "prefill: NULL tensor pointer");
+  REQUIRE(a->B >= 1 && a->T >= 0 && a->Hq >= 1 && a->Hkv >= 1 && a->max_seqlen >= 0, AFLEX_ERR_INVALID_ARG,
+          "prefill: need B, Hq, Hkv >= 1 and T, max_seqlen >= 0");
+  REQUIRE(a->Hq % a->Hkv == 0, AFLEX_ERR_INVALID_ARG, "prefill: Hq (%d) not a multiple of Hkv (%d)", a->Hq, a->Hkv);
+  REQUIRE(a->D == 128, AFLEX_ERR_UNSUPPORTED, "prefill: head_dim %d unsupported (128)", a->D);
+  REQUIRE(a->B <= 65535, AFLEX_ERR_UNSUPPORTED, "prefill: B %d above 65535", a->B);
+  REQUIRE(a->max_seqlen <= a->T, AFLEX_ERR_INVALID_ARG, "prefill: max_seqlen %d exceeds T %d", a->max_seqlen,
+          a->T);
+  REQUIRE(isfinite(a->scale) && a->scale >= 0.f, AFLEX_ERR_INVALID_ARG, "prefill: scale must be finite and >= 0");
+  REQUIRE(aligned16(a->q) && aligned16(a->k) && aligned16(a->v) && aligned16(a->out), AFLEX_ERR_ALIGNMENT,
+          "prefill: q, k, v and out must be 16-byte aligned");
+  REQUIRE(((uintptr_t)a->cu_seqlens & 3u) == 0, AFLEX_ERR_ALIGNMENT, "prefill: cu_seqlens must be 4-byte aligned");
+  return hip_status(aflex::launch_attn_prefill(*a, (hipStream_t)stream), "prefill");
+}
+
 static aflex_status check_linear(const aflex_linear_args* l) {
   REQUIRE(l, AFLEX_ERR_INVALID_ARG, "linear: args is NULL");
   REQUIRE(l->x && l->w && l->y, AFLEX_ERR_INVALID_ARG, "linear: NULL tensor pointer");

@@ -35,6 +35,9 @@ hipError_t launch_moe_route(const aflex_ffn_args& f, void* route_ws, hipStream_t
 hipError_t launch_moe_experts(const aflex_ffn_args& f, void* route_ws, void* expert_ws, hipStream_t stream,
                               const uint16_t* residual = nullptr);
 
+// Causal prefill attention (attn_prefill.hip).
+hipError_t launch_attn_prefill(const aflex_prefill_args& a, hipStream_t stream);
+
 // RMSNorm + router + MoE block (moe_block.hip).
 constexpr int kMaxRouterE = 64;
 size_t moe_block_workspace_bytes(const aflex_moe_block_args& m);

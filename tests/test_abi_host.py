@@ -21,7 +21,7 @@ def lib():
 
 def test_exports_every_declared_symbol(lib):
     names = aflex.exported_names()
-    assert len(names) == 17
+    assert len(names) == 18
     for n in names:
         assert hasattr(lib, n), n
     assert lib.aflex_version().startswith(b"aflex")
@@ -132,3 +132,31 @@ def test_pipeline_rejects(lib):
     assert lib.aflex_af_pipeline_step(ctypes.byref(a), ctypes.byref(f), 2, mb, 1,
                                       ctypes.c_void_p(FAKE), n.value - 1, None,
                                       ctypes.c_void_p(FAKE)) == aflex.ERR_WORKSPACE
+
+
+def _prefill(**kw):
+    a = aflex.PrefillArgs(q=FAKE, k=FAKE, v=FAKE, cu_seqlens=FAKE, out=FAKE, B=2, T=100, Hq=8, Hkv=2,
+                          D=128, max_seqlen=60, scale=0.0)
+    for k, v in kw.items():
+        setattr(a, k, v)
+    return a
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(q=None), aflex.ERR_INVALID_ARG),
+    (dict(cu_seqlens=None), aflex.ERR_INVALID_ARG),
+    (dict(B=0), aflex.ERR_INVALID_ARG),
+    (dict(T=-1), aflex.ERR_INVALID_ARG),
+    (dict(Hq=6, Hkv=4), aflex.ERR_INVALID_ARG),
+    (dict(D=64), aflex.ERR_UNSUPPORTED),
+    (dict(B=70000), aflex.ERR_UNSUPPORTED),
+    (dict(max_seqlen=101), aflex.ERR_INVALID_ARG),
+    (dict(max_seqlen=-1), aflex.ERR_INVALID_ARG),
+    (dict(scale=float("nan")), aflex.ERR_INVALID_ARG),
+    (dict(out=FAKE + 8), aflex.ERR_ALIGNMENT),
+    (dict(cu_seqlens=FAKE + 2), aflex.ERR_ALIGNMENT),
+])
+def test_prefill_validation(lib, kw, status):
+    a = _prefill(**kw)
+    assert lib.aflex_attn_prefill(ctypes.byref(a), None) == status
+    assert lib.aflex_last_error().startswith(b"prefill")
