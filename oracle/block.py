@@ -16,6 +16,8 @@ logits before the experts run (section 6.1 names the model):
     kv_append:  j = ctx_b - 1 (the new token is the last cached one)
                 K[table[b, j // bs], g, j % bs, :] = k_new[b, g, :]
                 V[table[b, j // bs], g, :, j % bs] = v_new[b, g, :]
+    kv_write:   the same for n_b new tokens per sequence (a prefilled prompt,
+                section 2: prefill populates the KV cache), j = ctx_b - n_b + i
     linear:     y = x W^T   (W in [out_features, in_features])
     rmsnorm:    x / sqrt(mean(x^2) + eps) * gamma
     moe_block:  y = MoE(RMSNorm(x), RMSNorm(x) W_r^T) (+ x with the residual)
@@ -43,6 +45,30 @@ def kv_append(k_cache, v_cache, block_table, context_lens, k_new, v_new):
         p = int(block_table[b, j // bs])
         k[p, :, j % bs, :] = k_new[b]
         v[p, :, :, j % bs] = v_new[b]
+    return k, v
+
+
+def kv_write(k_cache, v_cache, block_table, context_lens, cu_seqlens, k_new, v_new):
+    """Copies of the two pools with each sequence's new tokens written at the end
+    of its context: rows cu[b] .. cu[b+1]-1 of k_new / v_new are the n_b newest
+    tokens of sequence b, so token i lands at position ctx_b - n_b + i. A prompt
+    written by prefill has ctx_b = n_b (positions 0 .. n_b-1); one decode token
+    per sequence (n_b = 1) is kv_append. Positions below 0 (ctx_b < n_b) are not
+    written."""
+    k = k_cache.clone()
+    v = v_cache.clone()
+    bs = k.shape[2]
+    cu = [int(c) for c in cu_seqlens]
+    for b in range(len(cu) - 1):
+        n = cu[b + 1] - cu[b]
+        ctx = int(context_lens[b])
+        for i in range(n):
+            j = ctx - n + i
+            if j < 0:
+                continue
+            p = int(block_table[b, j // bs])
+            k[p, :, j % bs, :] = k_new[cu[b] + i]
+            v[p, :, :, j % bs] = v_new[cu[b] + i]
     return k, v
 
 

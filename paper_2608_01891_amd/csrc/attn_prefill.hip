@@ -22,7 +22,8 @@
 //                 swizzled by row so fragment reads are conflict-free).
 //   softmax       online, in the log2 domain: each lane holds 32 scores of
 //                 one query row (the accumulator's column), the other 32 sit
-//                 in lane l ^ 32; O is rescaled only when a row maximum moved.
+//                 in lane l ^ 32; O and l are rescaled only when a row's
+//                 maximum rises more than 2^8 above the reference maximum.
 //   O^T += V^T P^T  P^T is used straight from the S^T accumulator registers as
 //                 the B operand (rounded to bf16), which fixes the order of the
 //                 keys inside each 16-key k-step; V is transposed in registers
@@ -58,8 +59,10 @@ typedef float f32x8 __attribute__((ext_vector_type(8)));
 __device__ __forceinline__ void wait_vm8() { asm volatile("s_waitcnt vmcnt(8)" ::: "memory"); }
 __device__ __forceinline__ void wait_vm0() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
-// Byte offset of 16-byte chunk `chunk` of row `row` in the K tile (256-byte rows).
-__device__ __forceinline__ uint32_t k_off(int row, int chunk) { return row * 256 + ((chunk ^ (row & 7)) << 4); }
+// Byte offset of 16-byte chunk `chunk` of row `row` in the K tile (256-byte
+// rows, one 64-bank window each): 16 consecutive rows put a given chunk on 16
+// distinct bank groups.
+__device__ __forceinline__ uint32_t k_off(int row, int chunk) { return row * 256 + ((chunk ^ (row & 15)) << 4); }
 // Byte offset of 16-byte chunk `chunk` of row d in the V^T tile (128-byte rows).
 __device__ __forceinline__ uint32_t v_off(int d, int chunk) { return d * 128 + ((chunk ^ ((d + (d >> 3)) & 7)) << 4); }
 
@@ -100,24 +103,37 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_kernel(PrefillParams p) {
   const uint32_t ksm_lds = lds_offset(ksm);
 
   // K staging: wave-load i of thread tid fills slot i * 256 + tid, i.e. row
-  // (i * 256 + tid) / 16 and stored chunk tid % 16 of the tile.
+  // i * 16 + tid / 16 and stored chunk tid % 16 of the tile; the logical chunk
+  // is the same for all four wave-loads of a thread.
+  const int krow = tid >> 4, kchunk = (tid & 15) ^ krow;
+  const uint16_t* kp = kbase + (size_t)krow * kvstride + kchunk * 8;
   auto issue_k = [&](int kt, int buf) {
+    const uint32_t lds = ksm_lds + buf * 16384 + w * 1024;
+    if (kt * kPN + kPN <= n) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int row = i * 16 + (tid >> 4);
-      const int chunk = (tid & 15) ^ (row & 7);
-      const int key = min(kt * kPN + row, n - 1);
-      lds_dma16(kbase + (size_t)key * kvstride + chunk * 8, ksm_lds + buf * 16384 + i * 4096 + w * 1024);
+      for (int i = 0; i < 4; ++i) lds_dma16(kp + (size_t)(kt * kPN + i * 16) * kvstride, lds + i * 4096);
+    } else {  // tail tile: rows past the prompt re-read its last row (their scores are masked)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int key = min(kt * kPN + i * 16 + krow, n - 1);
+        lds_dma16(kbase + (size_t)key * kvstride + kchunk * 8, lds + i * 4096);
+      }
     }
   };
   // V staging: thread tid loads keys 4a .. 4a+3 (a = tid / 16) at d = 8 (tid % 16) + [0, 8).
   const int va = tid >> 4, vdc = tid & 15;
+  const uint16_t* vp = vbase + (size_t)(va * 4) * kvstride + vdc * 8;
   uint4 vr[4];
   auto load_v = [&](int kt) {
+    if (kt * kPN + kPN <= n) {
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int key = min(kt * kPN + va * 4 + j, n - 1);
-      vr[j] = *reinterpret_cast<const uint4*>(vbase + (size_t)key * kvstride + vdc * 8);
+      for (int j = 0; j < 4; ++j) vr[j] = *reinterpret_cast<const uint4*>(vp + (size_t)(kt * kPN + j) * kvstride);
+    } else {  // tail tile: rows past the prompt re-read its last row (their weights are 0)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int key = min(kt * kPN + va * 4 + j, n - 1);
+        vr[j] = *reinterpret_cast<const uint4*>(vbase + (size_t)key * kvstride + vdc * 8);
+      }
     }
   };
   // Keys 4a' .. 4a'+3 of a 16-key group sit at positions (a' % 2) * 8 + (a' / 2) * 4 + [0, 4)
@@ -193,22 +209,26 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_kernel(PrefillParams p) {
         }
     }
 
-    float mx = m_run;
+    float mx = kNegInf;
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
       for (int i = 0; i < 16; ++i) mx = fmaxf(mx, sacc[kb][i]);
     mx = fmaxf(mx, __shfl_xor(mx, 32));
-    if (__ballot(mx != m_run) != 0) {
-      const float alpha = fast_exp2((m_run - mx) * p.c);
+    // The reference maximum m_run only moves when a row's scores exceed it by
+    // more than 2^8 in the exponent: O and l share the reference, so the
+    // normalised result does not depend on it, and the weights stay <= 256.
+    if (__ballot((mx - m_run) * p.c > 8.f) != 0) {
+      const float mnew = fmaxf(m_run, mx);
+      const float alpha = fast_exp2((m_run - mnew) * p.c);
       l_run *= alpha;
 #pragma unroll
       for (int db = 0; db < kPD / 32; ++db)
 #pragma unroll
         for (int i = 0; i < 16; ++i) oacc[db][i] *= alpha;
-      m_run = mx;
+      m_run = mnew;
     }
-    const float mc = mx * p.c;
+    const float mc = m_run * p.c;
     float lsum = 0.f;
     bf16x8 pb[4];
 #pragma unroll

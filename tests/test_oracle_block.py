@@ -94,3 +94,44 @@ def test_moe_block_routes_on_normalised_coordinates_and_adds_residual():
     assert torch.allclose(y2 - y, x.double(), rtol=0, atol=1e-15)
     ref, _, _ = oracle.moe_ffn(xn, xn[:, :4], w.w_gate, w.w_up, w.w_down, 2)
     assert torch.equal(y, ref)
+
+
+def test_kv_write_one_token_each_is_kv_append():
+    a = synth.custom_attention(94, 4, 8, 2, 64, [1, 16, 17, 40], ctx_hi=48)
+    kn = torch.randn(4, 2, 64).to(torch.bfloat16)
+    vn = torch.randn(4, 2, 64).to(torch.bfloat16)
+    cu = torch.arange(5, dtype=torch.int32)
+    k1, v1 = oracle.kv_append(a.k_cache, a.v_cache, a.block_table, a.context_lens, kn, vn)
+    k2, v2 = oracle.kv_write(a.k_cache, a.v_cache, a.block_table, a.context_lens, cu, kn, vn)
+    assert torch.equal(k1, k2) and torch.equal(v1, v2)
+
+
+def test_kv_write_prefill_roundtrip_and_chunk_preserves_prefix():
+    ctx = [33, 16, 7, 0]
+    a = synth.custom_attention(95, 4, 4, 2, 16, ctx, ctx_hi=48)
+    new = [33, 16, 3, 0]                 # prompts, a full-block prompt, a 3-token chunk, nothing
+    cu = torch.tensor([0] + list(np.cumsum(new)), dtype=torch.int32)
+    T = int(cu[-1])
+    kn = torch.randn(T, 2, 16).to(torch.bfloat16)
+    vn = torch.randn(T, 2, 16).to(torch.bfloat16)
+    k, v = oracle.kv_write(a.k_cache, a.v_cache, a.block_table, a.context_lens, cu, kn, vn)
+    for b, (c, n) in enumerate(zip(ctx, new)):
+        kg, vg = oracle.gather_sequence(k, v, a.block_table, b, c)
+        k0, v0 = oracle.gather_sequence(a.k_cache, a.v_cache, a.block_table, b, c)
+        s0 = int(cu[b])
+        assert torch.equal(kg[:, c - n:], kn[s0:s0 + n].permute(1, 0, 2).double())
+        assert torch.equal(vg[:, c - n:], vn[s0:s0 + n].permute(1, 0, 2).double())
+        assert torch.equal(kg[:, :c - n], k0[:, :c - n]) and torch.equal(vg[:, :c - n], v0[:, :c - n])
+    touched = int((k != a.k_cache).any(dim=(1, 3)).sum())
+    assert touched == sum(new)
+
+
+def test_prefill_write_then_decode_equals_prefill_last_row():
+    lens = [21, 16]
+    p = synth.make_prefill(96, lens, 4, 2, 16)
+    a = synth.custom_attention(96, 2, 4, 2, 16, lens, ctx_hi=32)
+    k, v = oracle.kv_write(a.k_cache, a.v_cache, a.block_table, a.context_lens, p.cu_seqlens, p.k, p.v)
+    last = (p.cu_seqlens[1:] - 1).long()
+    dec = oracle.attention_decode(p.q[last], k, v, a.block_table, a.context_lens)
+    pre = oracle.attention_prefill(p.q, p.k, p.v, p.cu_seqlens)
+    assert torch.allclose(dec, pre[last], rtol=1e-12, atol=1e-13)
