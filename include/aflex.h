@@ -190,6 +190,33 @@ typedef struct aflex_kv_append_args {
 /* Supported: D in {64, 128}, block_size == 16. No workspace. */
 aflex_status aflex_kv_append(const aflex_kv_append_args *a, aflex_stream stream);
 
+/* Packed multi-token KV-cache write: prefill populates the cache with the     */
+/* prompt's keys and values (section 2, "LLM Serving"), and chunked prefill    */
+/* appends a chunk. Sequence b's new tokens are rows cu_seqlens[b] ..          */
+/* cu_seqlens[b+1]-1 of k_new / v_new and are the newest n_b cached tokens:    */
+/* token i goes to position context_lens[b] - n_b + i (positions below 0 are   */
+/* skipped). With one token per sequence this is aflex_kv_append.             */
+typedef struct aflex_kv_write_args {
+  const aflex_bf16 *k_new;     /* [T, Hkv, D] */
+  const aflex_bf16 *v_new;     /* [T, Hkv, D] */
+  const int32_t *cu_seqlens;   /* [B+1] device, nondecreasing, cu[0] = 0, cu[B] = T */
+  aflex_bf16 *k_cache;         /* [num_blocks, Hkv, block_size, D] (written) */
+  aflex_bf16 *v_cache;         /* [num_blocks, Hkv, D, block_size] (written) */
+  const int32_t *block_table;  /* [B, max_blocks_per_seq] */
+  const int32_t *context_lens; /* [B], cached tokens after the write */
+  int32_t B, T, Hkv, D;
+  int32_t max_seqlen;          /* host-known bound on n_b; sizes the grid */
+  int32_t block_size;          /* must be 16 */
+  int32_t max_blocks_per_seq, num_blocks;
+} aflex_kv_write_args;
+
+/* Supported: D in {64, 128}, block_size == 16, Hkv * D / 8 <= 1024,          */
+/* B <= 65535. No workspace. Device-side values are clamped: prompts to       */
+/* [0, T], sequences with context_lens outside [1, capacity] and block ids    */
+/* outside [0, num_blocks) write nothing; tokens of a sequence longer than    */
+/* max_seqlen beyond the grid's reach are not written.                         */
+aflex_status aflex_kv_write(const aflex_kv_write_args *a, aflex_stream stream);
+
 /* Linear layer y = x W^T in bf16 with fp32 accumulation: the output           */
 /* projection that brings the attention output back to the hidden size        */
 /* before it crosses the A/F boundary (section 4.3).                           */
@@ -237,10 +264,10 @@ aflex_status aflex_attn_prefill(const aflex_prefill_args *a, aflex_stream stream
 /* name is in the comma-separated list `kernels` (NULL or "" = all) is        */
 /* bracketed by two HIP events on the stream it is launched on. Kernel names: */
 /* attn_split, attn_merge, gemm_gate_up, gemm_down, splitk_reduce, moe_route, */
-/* moe_combine, kv_append, rmsnorm_router, attn_prefill. aflex_profile_stop */
-/* waits for those events and writes one line per kernel into `report`      */
-/* (host buffer of `len` bytes, truncated to fit):                           */
-/*   <name> <launches> <total_ms> <min_ms> <max_ms>                          */
+/* moe_combine, kv_append, kv_write, rmsnorm_router, attn_prefill.            */
+/* aflex_profile_stop waits for those events and writes one line per kernel   */
+/* into `report` (host buffer of `len` bytes, truncated to fit):              */
+/*   <name> <launches> <total_ms> <min_ms> <max_ms>                           */
 /* Off by default; while off no event is recorded.                            */
 /* ------------------------------------------------------------------------ */
 aflex_status aflex_profile_start(const char *kernels);

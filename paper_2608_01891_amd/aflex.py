@@ -54,6 +54,13 @@ class MoeBlockArgs(ctypes.Structure):
                 ("eps", ctypes.c_float), ("residual", _i), ("router_logits_out", _p)]
 
 
+class KvWriteArgs(ctypes.Structure):
+    _fields_ = [("k_new", _p), ("v_new", _p), ("cu_seqlens", _p), ("k_cache", _p), ("v_cache", _p),
+                ("block_table", _p), ("context_lens", _p),
+                ("B", _i), ("T", _i), ("Hkv", _i), ("D", _i), ("max_seqlen", _i), ("block_size", _i),
+                ("max_blocks_per_seq", _i), ("num_blocks", _i)]
+
+
 class PrefillArgs(ctypes.Structure):
     _fields_ = [("q", _p), ("k", _p), ("v", _p), ("cu_seqlens", _p), ("out", _p),
                 ("B", _i), ("T", _i), ("Hq", _i), ("Hkv", _i), ("D", _i),
@@ -102,6 +109,7 @@ def load():
         "aflex_linear_workspace": [ctypes.POINTER(LinearArgs), _SZ],
         "aflex_linear": [ctypes.POINTER(LinearArgs), _p, ctypes.c_size_t, _p],
         "aflex_attn_prefill": [ctypes.POINTER(PrefillArgs), _p],
+        "aflex_kv_write": [ctypes.POINTER(KvWriteArgs), _p],
     }
     for name, args in sig.items():
         fn = getattr(lib, name)
@@ -247,6 +255,22 @@ def kv_append(a, k_new, v_new, stream=None):
                         block_size=a.block_size, max_blocks_per_seq=a.max_blocks,
                         num_blocks=a.num_blocks)
     _check(lib.aflex_kv_append(ctypes.byref(args), _stream(stream)))
+
+
+def kv_write(a, k_new, v_new, cu_seqlens, max_seqlen=None, stream=None):
+    """Write packed new tokens (rows cu[b] .. cu[b+1]-1 for sequence b) at the end of each
+    sequence's context in a's paged pools, in place."""
+    lib = load()
+    T = k_new.shape[0]
+    if max_seqlen is None:
+        c = cu_seqlens.cpu()
+        max_seqlen = int((c[1:] - c[:-1]).max()) if c.numel() > 1 else 0
+    args = KvWriteArgs(k_new=_ptr(k_new), v_new=_ptr(v_new), cu_seqlens=_ptr(cu_seqlens),
+                       k_cache=_ptr(a.k_cache), v_cache=_ptr(a.v_cache), block_table=_ptr(a.block_table),
+                       context_lens=_ptr(a.context_lens), B=a.B, T=T, Hkv=a.Hkv, D=a.D,
+                       max_seqlen=max_seqlen, block_size=a.block_size, max_blocks_per_seq=a.max_blocks,
+                       num_blocks=a.num_blocks)
+    _check(lib.aflex_kv_write(ctypes.byref(args), _stream(stream)))
 
 
 def attn_prefill(p, out=None, max_seqlen=None, scale: float = 0.0, stream=None):

@@ -190,6 +190,26 @@ aflex_status aflex_kv_append(const aflex_kv_append_args* a, aflex_stream stream)
   return hip_status(aflex::launch_kv_append(*a, (hipStream_t)stream), "kv_append");
 }
 
+aflex_status aflex_kv_write(const aflex_kv_write_args* a, aflex_stream stream) {
+  REQUIRE(a, AFLEX_ERR_INVALID_ARG, "kv_write: args is NULL");
+  REQUIRE(a->k_new && a->v_new && a->cu_seqlens && a->k_cache && a->v_cache && a->block_table && a->context_lens,
+          AFLEX_ERR_INVALID_ARG, "kv_write: NULL tensor pointer");
+  REQUIRE(a->B >= 1 && a->T >= 0 && a->Hkv >= 1 && a->num_blocks >= 1 && a->max_blocks_per_seq >= 1 &&
+              a->max_seqlen >= 0,
+          AFLEX_ERR_INVALID_ARG, "kv_write: need B, Hkv, num_blocks, max_blocks_per_seq >= 1 and T, max_seqlen >= 0");
+  REQUIRE(a->max_seqlen <= a->T, AFLEX_ERR_INVALID_ARG, "kv_write: max_seqlen %d exceeds T %d", a->max_seqlen, a->T);
+  REQUIRE(a->D == 64 || a->D == 128, AFLEX_ERR_UNSUPPORTED, "kv_write: head_dim %d unsupported (64 or 128)", a->D);
+  REQUIRE(a->block_size == 16, AFLEX_ERR_UNSUPPORTED, "kv_write: block_size %d unsupported (16)", a->block_size);
+  REQUIRE(a->Hkv * (a->D / 8) <= 1024 && a->B <= 65535, AFLEX_ERR_UNSUPPORTED,
+          "kv_write: Hkv * D / 8 must be <= 1024 and B <= 65535");
+  REQUIRE(aligned16(a->k_new) && aligned16(a->v_new) && aligned16(a->k_cache) && aligned16(a->v_cache),
+          AFLEX_ERR_ALIGNMENT, "kv_write: tensors must be 16-byte aligned");
+  REQUIRE(((uintptr_t)a->cu_seqlens & 3u) == 0 && ((uintptr_t)a->block_table & 3u) == 0 &&
+              ((uintptr_t)a->context_lens & 3u) == 0,
+          AFLEX_ERR_ALIGNMENT, "kv_write: index arrays must be 4-byte aligned");
+  return hip_status(aflex::launch_kv_write(*a, (hipStream_t)stream), "kv_write");
+}
+
 aflex_status aflex_attn_prefill(const aflex_prefill_args* a, aflex_stream stream) {
   REQUIRE(a, AFLEX_ERR_INVALID_ARG, "prefill: args is NULL");
   REQUIRE(a->q && a->k && a->v && a->cu_seqlens && a->out, AFLEX_ERR_INVALID_ARG, "prefill: NULL tensor pointer");

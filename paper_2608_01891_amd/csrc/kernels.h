@@ -20,6 +20,7 @@ hipError_t launch_swiglu(const aflex_ffn_args& f, void* ws, hipStream_t stream);
 
 // KV-cache append (kv_append.hip) and linear layer (ffn.hip).
 hipError_t launch_kv_append(const aflex_kv_append_args& a, hipStream_t stream);
+hipError_t launch_kv_write(const aflex_kv_write_args& a, hipStream_t stream);
 size_t linear_workspace_bytes(const aflex_linear_args& l);
 hipError_t launch_linear(const aflex_linear_args& l, void* ws, hipStream_t stream);
 

@@ -331,6 +331,11 @@ def prefill_workload(model: str = "qwen3-32b", prompt_len: int = 4096, prompts: 
     return make_prefill(seed, [prompt_len] * prompts, Hq, Hkv, D, device=device)
 
 
+def prefill_ffn_tokens(H: int, T: int, device="cpu") -> torch.Tensor:
+    """FFN input [T, H] of a prefill batch (all prompt tokens at once)."""
+    return normal_tensor(7, STREAM["x"], (T, H), device=device)
+
+
 def custom_attention(seed: int, B: int, Hq: int, Hkv: int, D: int, ctx, ctx_hi: int | None = None,
                      device="cpu") -> AttnInputs:
     """Attention inputs with given context lengths (tests: edge cases, ragged tails)."""

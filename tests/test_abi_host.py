@@ -21,7 +21,7 @@ def lib():
 
 def test_exports_every_declared_symbol(lib):
     names = aflex.exported_names()
-    assert len(names) == 18
+    assert len(names) == 19
     for n in names:
         assert hasattr(lib, n), n
     assert lib.aflex_version().startswith(b"aflex")
@@ -160,3 +160,20 @@ def test_prefill_validation(lib, kw, status):
     a = _prefill(**kw)
     assert lib.aflex_attn_prefill(ctypes.byref(a), None) == status
     assert lib.aflex_last_error().startswith(b"prefill")
+
+
+def test_kv_write_validation(lib):
+    def mk(**kw):
+        a = aflex.KvWriteArgs(k_new=FAKE, v_new=FAKE, cu_seqlens=FAKE, k_cache=FAKE, v_cache=FAKE,
+                              block_table=FAKE, context_lens=FAKE, B=2, T=40, Hkv=2, D=128, max_seqlen=30,
+                              block_size=16, max_blocks_per_seq=4, num_blocks=8)
+        for k, v in kw.items():
+            setattr(a, k, v)
+        return a
+    for kw, st in [(dict(k_new=None), aflex.ERR_INVALID_ARG), (dict(max_seqlen=41), aflex.ERR_INVALID_ARG),
+                   (dict(D=96), aflex.ERR_UNSUPPORTED), (dict(block_size=8), aflex.ERR_UNSUPPORTED),
+                   (dict(Hkv=65), aflex.ERR_UNSUPPORTED), (dict(v_cache=FAKE + 4), aflex.ERR_ALIGNMENT),
+                   (dict(cu_seqlens=FAKE + 1), aflex.ERR_ALIGNMENT)]:
+        a = mk(**kw)
+        assert lib.aflex_kv_write(ctypes.byref(a), None) == st, kw
+        assert lib.aflex_last_error().startswith(b"kv_write")

@@ -42,3 +42,14 @@ def test_qwen3_shape_sampled(gpu_lib, qwen3_weights, T):
     check_rows(y[rows], ref, what=f"qwen3 swiglu T={T} (sampled)")
     y2 = aflex.ffn_swiglu(wl.x, w).cpu()
     assert torch.equal(y, y2)
+
+
+def test_qwen3_prefill_tokens_sampled(gpu_lib, qwen3_weights):
+    """The dense FFN over a prefill batch: two 2048-token prompts at once (T = 4096)."""
+    w, (wg, wu, wd) = qwen3_weights
+    T = 4096
+    x = synth.prefill_ffn_tokens(5120, T, device=DEV)
+    y = aflex.ffn_swiglu(x, w).cpu()
+    rows = sample_rows(T, 6, seed=T, must=[0, 255, 256, T - 1])
+    ref = oracle.swiglu_ffn(x[rows].cpu(), wg, wu, wd)
+    check_rows(y[rows], ref, what="qwen3 swiglu prefill T=4096 (sampled)")

@@ -76,3 +76,16 @@ def test_mixtral_shape(gpu_lib, mixtral):
     check_rows(y[toks], ref[toks], what="mixtral moe (sampled)")
     y2 = aflex.moe_ffn(wl.x, wl.ffn, wl.router_logits, 2).cpu()
     assert torch.equal(y, y2)
+
+
+def test_mixtral_prefill_tokens_sampled(gpu_lib, mixtral):
+    """The MoE FFN over a prefill batch (T = 4096 tokens, 8192 token/slot pairs)."""
+    T = 4096
+    wl = synth.mixtral_moe(device=DEV, T=T, seed=7, weights=mixtral.ffn)
+    y, r = aflex.moe_ffn(wl.x, wl.ffn, wl.router_logits, 2, routing=True)
+    _check_routing(r, wl.router_logits, 2, 8)
+    toks = sample_rows(T, 6, seed=7, must=[0, T - 1])
+    f = wl.ffn
+    ref, _, _ = oracle.moe_ffn(wl.x.cpu(), wl.router_logits.cpu(), f.w_gate.cpu(), f.w_up.cpu(),
+                               f.w_down.cpu(), 2, token_indices=toks)
+    check_rows(y.cpu()[toks], ref[toks], what="mixtral moe prefill T=4096 (sampled)")

@@ -65,3 +65,50 @@ def test_paper_prompt_lengths_sampled(gpu_lib, model, prompt_len, prompts):
                        must=[0, 1, 127, 128, prompt_len - 1, T - 1, T - prompt_len])
     ref = oracle.attention_prefill(pc.q, pc.k, pc.v, pc.cu_seqlens, rows=rows)
     check_rows(out[rows], ref[rows], what=f"{model} prefill {prompts}x{prompt_len} (sampled)")
+
+
+def _cu(new):
+    return torch.tensor([0] + [int(x) for x in torch.tensor(new).cumsum(0)], dtype=torch.int32)
+
+
+@pytest.mark.parametrize("D,ctx,new", [
+    (128, [33, 16, 7, 0, 200, 1], [33, 16, 3, 0, 190, 1]),   # prompts, full block, chunks, empty
+    (64, [5, 48, 100], [5, 20, 100]),
+])
+def test_kv_write_bit_exact(gpu_lib, D, ctx, new):
+    a = synth.custom_attention(99, len(ctx), 8, 2, D, ctx, ctx_hi=max(ctx) + 20)
+    cu = _cu(new)
+    T = int(cu[-1])
+    kn = synth.normal_tensor(99, 42, (T, 2, D))
+    vn = synth.normal_tensor(99, 43, (T, 2, D))
+    rk, rv = oracle.kv_write(a.k_cache, a.v_cache, a.block_table, a.context_lens, cu, kn, vn)
+    ad = a.to(DEV)
+    aflex.kv_write(ad, kn.to(DEV), vn.to(DEV), cu.to(DEV), max_seqlen=max(new))
+    assert torch.equal(ad.k_cache.cpu(), rk) and torch.equal(ad.v_cache.cpu(), rv)
+
+
+def test_kv_write_one_token_each_matches_kv_append(gpu_lib):
+    ctx = [1, 15, 16, 17, 700]
+    a = synth.custom_attention(100, len(ctx), 8, 2, 128, ctx, ctx_hi=720)
+    kn = synth.normal_tensor(100, 42, (len(ctx), 2, 128)).to(DEV)
+    vn = synth.normal_tensor(100, 43, (len(ctx), 2, 128)).to(DEV)
+    a1, a2 = a.to(DEV), a.to(DEV)
+    aflex.kv_append(a1, kn, vn)
+    aflex.kv_write(a2, kn, vn, torch.arange(len(ctx) + 1, dtype=torch.int32, device=DEV), max_seqlen=1)
+    assert torch.equal(a1.k_cache, a2.k_cache) and torch.equal(a1.v_cache, a2.v_cache)
+
+
+def test_prefill_then_decode_on_the_written_cache(gpu_lib):
+    """A prefill pass writes the prompts into the paged cache; decode attention
+    for each prompt's last token over that cache equals the prefill output row."""
+    lens = [300, 17, 128]
+    p = synth.make_prefill(101, lens, 16, 2, 128, device=DEV)
+    a = synth.custom_attention(101, len(lens), 16, 2, 128, lens, ctx_hi=320).to(DEV)
+    aflex.kv_write(a, p.k, p.v, p.cu_seqlens, max_seqlen=max(lens))
+    out = aflex.attn_prefill(p).cpu()
+    last = (p.cu_seqlens[1:] - 1).long().cpu()
+    a.q = p.q[last.to(DEV)].contiguous()
+    dec = aflex.attn_decode(a).cpu()
+    ref = oracle.attention_prefill(p.q.cpu(), p.k.cpu(), p.v.cpu(), p.cu_seqlens.cpu(), rows=last.tolist())
+    check_rows(dec, ref[last], what="decode over the prefilled cache")
+    check_rows(out[last], ref[last], what="prefill last rows")
