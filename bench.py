@@ -436,6 +436,62 @@ def main():
                     "tok_per_s": round(T / (ms_b * 1e-3), 1),
                     "kernels": {kname: round(v[1] / v[0], 5) for kname, v in kp.items()}}
             del wm
+
+        # Prefill (the paper's PA and PF operators, section 3.2), at its two prompt
+        # lengths (128 and 4096 tokens, section 6.1): causal attention over packed
+        # prompts, the KV-cache write of the prompts, and the FFNs over all
+        # prompt tokens at once.
+        for model, plen, nprompt in (("qwen3-32b", 4096, 2), ("qwen3-32b", 128, 32), ("mixtral-8x7b", 4096, 2)):
+            pw = synth.prefill_workload(model, plen, nprompt, device=dev)
+            outp = aflex.attn_prefill(pw)
+            aflex.profile_start(["attn_prefill"])
+            ms = timed(lambda: aflex.attn_prefill(pw, out=outp), 10)
+            kp = aflex.profile_stop()
+            pflops = sum(4.0 * n * (n + 1) / 2 * pw.Hq * pw.D for n in pw.lens)
+            tag = f"prefill_attention_{model.split('-')[0]}_{nprompt}x{plen}"
+            ops[tag] = {"ms": round(ms, 5), "tflops": round(pflops / (ms * 1e-3) / 1e12, 1),
+                        "mfma_frac": round(pflops / (ms * 1e-3) / PEAK_BF16, 4),
+                        "tok_per_s": round(pw.T / (ms * 1e-3), 1),
+                        "kernels": {kname: round(v[1] / v[0], 5) for kname, v in kp.items()}}
+            if plen == 4096 and model == "qwen3-32b":
+                pc = synth.custom_attention(5, nprompt, pw.Hq, pw.Hkv, pw.D, pw.lens).to(dev)
+                aflex.kv_write(pc, pw.k, pw.v, pw.cu_seqlens, max_seqlen=plen)
+                aflex.profile_start(["kv_write"])
+                ms = timed(lambda: aflex.kv_write(pc, pw.k, pw.v, pw.cu_seqlens, max_seqlen=plen), 10)
+                kp = aflex.profile_stop()
+                kvb = 2 * 2 * pw.k.numel() * 2
+                ops[f"kv_write_qwen3_{nprompt}x{plen}"] = {
+                    "ms": round(ms, 5), "GB_per_s": round(kvb / (ms * 1e-3) / 1e9, 1),
+                    "hbm_frac": round(kvb / (ms * 1e-3) / PEAK_HBM, 4), "bytes": kvb,
+                    "kernels": {kname: round(v[1] / v[0], 5) for kname, v in kp.items()}}
+                del pc
+            del pw, outp
+        Tp = 4096
+        wd = synth.make_ffn_weights(2, 5120, 25600, device=dev)
+        xp = synth.prefill_ffn_tokens(5120, Tp, device=dev)
+        yp = torch.empty(Tp, 5120, dtype=torch.bfloat16, device=dev)
+        aflex.ffn_swiglu(xp, wd, y=yp)
+        aflex.profile_start(["gemm_gate_up", "gemm_down", "splitk_reduce"])
+        ms = timed(lambda: aflex.ffn_swiglu(xp, wd, y=yp), 5)
+        kp = aflex.profile_stop()
+        flops = 6 * Tp * 5120 * 25600
+        ops[f"prefill_swiglu_qwen3_T{Tp}"] = {
+            "ms": round(ms, 5), "tflops": round(flops / (ms * 1e-3) / 1e12, 1),
+            "mfma_frac": round(flops / (ms * 1e-3) / PEAK_BF16, 4), "tok_per_s": round(Tp / (ms * 1e-3), 1),
+            "kernels": {kname: round(v[1] / v[0], 5) for kname, v in kp.items()}}
+        del wd, xp, yp
+        wm = synth.mixtral_moe(device=dev, T=Tp, seed=7, weights=f)
+        yp = torch.empty(Tp, H, dtype=torch.bfloat16, device=dev)
+        aflex.moe_ffn(wm.x, wm.ffn, wm.router_logits, 2, y=yp)
+        aflex.profile_start(None)
+        ms = timed(lambda: aflex.moe_ffn(wm.x, wm.ffn, wm.router_logits, 2, y=yp), 5)
+        kp = aflex.profile_stop()
+        flops = Tp * 2 * 6 * H * I
+        ops[f"prefill_moe_mixtral_T{Tp}"] = {
+            "ms": round(ms, 5), "tflops": round(flops / (ms * 1e-3) / 1e12, 1),
+            "mfma_frac": round(flops / (ms * 1e-3) / PEAK_BF16, 4), "tok_per_s": round(Tp / (ms * 1e-3), 1),
+            "kernels": {kname: round(v[1] / v[0], 5) for kname, v in kp.items()}}
+        del wm, yp
         result["operators"] = ops
 
     # ---------------- CPU baseline: the oracle on a bounded sample -------------------
