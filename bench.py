@@ -83,6 +83,22 @@ def energy_reader():
         return None
 
 
+def clock_reader():
+    """Callable returning the current graphics clock in MHz, or None."""
+    try:
+        import amdsmi
+        amdsmi.amdsmi_init()
+        h = amdsmi.amdsmi_get_processor_handles()[0]
+
+        def read():
+            c = amdsmi.amdsmi_get_clock_info(h, amdsmi.AmdSmiClkType.GFX)
+            return float(c.get("clk", c.get("cur_clk")))
+        read()
+        return read
+    except Exception:
+        return None
+
+
 def topk_ids_host(logits, k):
     import numpy as np
     return np.argsort(-logits, axis=1, kind="stable")[:, :k]
@@ -226,16 +242,25 @@ def main():
 
     # ---------------- energy per token (where the counter is readable) -------------
     read_energy = energy_reader()
+    read_clock = clock_reader()
     if read_energy is not None:
         n = max(1, int(1.5 / (ms_step * 1e-3)))
         torch.cuda.synchronize()
         e0, t0 = read_energy(), time.perf_counter()
         for _ in range(n):
             step()
+        clocks = []
+        if read_clock is not None:  # sampled while the queued steps run
+            for _ in range(10):
+                time.sleep(0.05)
+                clocks.append(read_clock())
         torch.cuda.synchronize()
         e1, t1 = read_energy(), time.perf_counter()
         result["energy"] = {"joules_per_token": round((e1 - e0) / (n * B), 6),
                             "avg_watts": round((e1 - e0) / (t1 - t0), 1), "steps": n}
+        if clocks:
+            result["energy"]["gfx_clock_mhz"] = {"min": min(clocks), "max": max(clocks),
+                                                 "mean": round(sum(clocks) / len(clocks), 1)}
     else:
         result["energy"] = "n/a (energy counter not readable)"
 
@@ -520,8 +545,10 @@ def main():
 
         n_seq = 8
         dt, ntok = oracle_sample(n_seq)
-        if dt < 5.0:  # grow the sample towards ~15 s of oracle work
-            n_seq = min(B, max(n_seq, int(n_seq * 15.0 / max(dt, 1e-3))))
+        for _ in range(2):  # grow the sample towards ~15 s of oracle work (at most the whole batch)
+            if dt >= 10.0 or n_seq >= B:
+                break
+            n_seq = min(B, max(n_seq + 1, int(n_seq * 15.0 / max(dt, 1e-3))))
             dt, ntok = oracle_sample(n_seq)
         result["cpu_baseline"] = {
             "value": round(n_seq / dt, 4), "unit": "tok/s", "cores": torch.get_num_threads(),
