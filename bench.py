@@ -66,6 +66,16 @@ def timed(fn, reps, stream=None):
     return e0.elapsed_time(e1) / reps
 
 
+def timed_kernels(fn, reps, names, aflex):
+    """(ms per call without profiling events, {kernel: avg ms} from a separate profiled pass)."""
+    ms = timed(fn, reps)
+    aflex.profile_start(names)
+    for _ in range(max(3, reps // 3)):
+        fn()
+    kp = aflex.profile_stop()
+    return ms, {kname: round(v[1] / v[0], 5) for kname, v in kp.items()}
+
+
 def energy_reader():
     """Callable returning the GPU's accumulated energy in joules, or None."""
     try:
@@ -358,14 +368,12 @@ def main():
             it[0] += 1
         for _ in range(3):
             run_attn()
-        aflex.profile_start(["attn_split", "attn_merge"])
-        ms = timed(run_attn, 30)
-        kp = aflex.profile_stop()
+        ms, kk = timed_kernels(run_attn, 30, ["attn_split", "attn_merge"], aflex)
         ops["attention_qwen3_B64"] = {
             "ms": round(ms, 5), "GB_per_s": round(abytes / (ms * 1e-3) / 1e9, 1),
             "hbm_frac": round(abytes / (ms * 1e-3) / PEAK_HBM, 4), "bytes": abytes,
             "tflops": round(aflops / (ms * 1e-3) / 1e12, 2), "tok_per_s": round(wq.B / (ms * 1e-3), 1),
-            "kernels": {kname: round(v[1] / v[0], 5) for kname, v in kp.items()}}
+            "kernels": kk}
         # The whole attention stage of a Qwen3 decode layer: KV append of the new
         # token, attention, output projection [64, 8192] x [5120, 8192]^T.
         kn = synth.normal_tensor(1, 40, (wq.B, wq.Hkv, wq.D), device=dev)
@@ -382,15 +390,13 @@ def main():
             it[0] += 1
         for _ in range(3):
             run_stage()
-        aflex.profile_start(["kv_append", "attn_split", "attn_merge", "gemm_down", "splitk_reduce"])
-        ms = timed(run_stage, 30)
-        kp = aflex.profile_stop()
+        ms, kk = timed_kernels(run_stage, 30, ["kv_append", "attn_split", "attn_merge", "gemm_down", "splitk_reduce"], aflex)
         sbytes = abytes + w_o.numel() * 2 + 2 * wq.B * 5120 * 2 + 2 * kn.numel() * 2
         ops["attention_stage_qwen3_B64"] = {
             "ms": round(ms, 5), "GB_per_s": round(sbytes / (ms * 1e-3) / 1e9, 1),
             "hbm_frac": round(sbytes / (ms * 1e-3) / PEAK_HBM, 4), "bytes": sbytes,
             "tok_per_s": round(wq.B / (ms * 1e-3), 1),
-            "kernels": {kname: round(v[1] / v[0], 5) for kname, v in kp.items()}}
+            "kernels": kk}
         del copies, wq, w_o
 
         # Full-batch long-context attention of the pipeline workload
@@ -408,9 +414,7 @@ def main():
             wlT = synth.qwen3_swiglu(T, device=dev, weights=wd)
             yT = torch.empty(T, 5120, dtype=torch.bfloat16, device=dev)
             aflex.ffn_swiglu(wlT.x, wd, y=yT)
-            aflex.profile_start(["gemm_gate_up", "gemm_down", "splitk_reduce"])
-            ms = timed(lambda: aflex.ffn_swiglu(wlT.x, wd, y=yT), 10)
-            kp = aflex.profile_stop()
+            ms, kk = timed_kernels(lambda: aflex.ffn_swiglu(wlT.x, wd, y=yT), 10, ["gemm_gate_up", "gemm_down", "splitk_reduce"], aflex)
             flops = 6 * T * 5120 * 25600
             byts = 3 * 5120 * 25600 * 2 + 2 * T * 5120 * 2
             att = min(PEAK_BF16, flops / byts * PEAK_HBM)
@@ -421,7 +425,7 @@ def main():
                 "GB_per_s": round(byts / (ms * 1e-3) / 1e9, 1),
                 "hbm_frac": round(byts / (ms * 1e-3) / PEAK_HBM, 4),
                 "tok_per_s": round(T / (ms * 1e-3), 1),
-                "kernels": {kname: round(v[1] / v[0], 5) for kname, v in kp.items()}}
+                "kernels": kk}
         del wd
 
         # Mixtral MoE, T = 256 (and T = 2048 supplementary)
@@ -429,9 +433,7 @@ def main():
             wm = synth.mixtral_moe(device=dev, T=T, seed=seed, weights=f if T == 2048 else None)
             yT = torch.empty(T, H, dtype=torch.bfloat16, device=dev)
             aflex.moe_ffn(wm.x, wm.ffn, wm.router_logits, 2, y=yT)
-            aflex.profile_start(None)
-            ms = timed(lambda: aflex.moe_ffn(wm.x, wm.ffn, wm.router_logits, 2, y=yT), 10)
-            kp = aflex.profile_stop()
+            ms, kk = timed_kernels(lambda: aflex.moe_ffn(wm.x, wm.ffn, wm.router_logits, 2, y=yT), 10, None, aflex)
             ids = topk_ids_host(wm.router_logits.cpu().numpy(), 2)
             touched = len(np.unique(ids))
             flops = T * 2 * 6 * H * I
@@ -444,22 +446,20 @@ def main():
                 "GB_per_s": round(byts / (ms * 1e-3) / 1e9, 1),
                 "hbm_frac": round(byts / (ms * 1e-3) / PEAK_HBM, 4),
                 "tok_per_s": round(T / (ms * 1e-3), 1),
-                "kernels": {kname: round(v[1] / v[0], 5) for kname, v in kp.items()}}
+                "kernels": kk}
             if T == 256:
                 # the whole MoE FFN block: RMSNorm, router GEMM, experts, residual
                 gamma = (1.0 + 0.1 * synth.normal_tensor(seed, 50, (H,), dtype=torch.float32,
                                                          device=dev)).to(torch.bfloat16)
                 wr = synth.normal_tensor(seed, 51, (8, H), scale=0.02, device=dev)
                 aflex.moe_block(wm.x, wm.ffn, gamma, wr, 2, residual=True, y=yT)
-                aflex.profile_start(["rmsnorm_router"])
-                ms_b = timed(lambda: aflex.moe_block(wm.x, wm.ffn, gamma, wr, 2, residual=True,
-                                                     y=yT), 10)
-                kp = aflex.profile_stop()
+                ms_b, kk = timed_kernels(lambda: aflex.moe_block(wm.x, wm.ffn, gamma, wr, 2, residual=True,
+                                                     y=yT), 10, ["rmsnorm_router"], aflex)
                 ops["moe_block_mixtral_T256"] = {
                     "ms": round(ms_b, 5), "GB_per_s": round(byts / (ms_b * 1e-3) / 1e9, 1),
                     "hbm_frac": round(byts / (ms_b * 1e-3) / PEAK_HBM, 4),
                     "tok_per_s": round(T / (ms_b * 1e-3), 1),
-                    "kernels": {kname: round(v[1] / v[0], 5) for kname, v in kp.items()}}
+                    "kernels": kk}
             del wm
 
         # Prefill (the paper's PA and PF operators, section 3.2), at its two prompt
@@ -469,26 +469,22 @@ def main():
         for model, plen, nprompt in (("qwen3-32b", 4096, 2), ("qwen3-32b", 128, 32), ("mixtral-8x7b", 4096, 2)):
             pw = synth.prefill_workload(model, plen, nprompt, device=dev)
             outp = aflex.attn_prefill(pw)
-            aflex.profile_start(["attn_prefill"])
-            ms = timed(lambda: aflex.attn_prefill(pw, out=outp), 10)
-            kp = aflex.profile_stop()
+            ms, kk = timed_kernels(lambda: aflex.attn_prefill(pw, out=outp), 10, ["attn_prefill"], aflex)
             pflops = sum(4.0 * n * (n + 1) / 2 * pw.Hq * pw.D for n in pw.lens)
             tag = f"prefill_attention_{model.split('-')[0]}_{nprompt}x{plen}"
             ops[tag] = {"ms": round(ms, 5), "tflops": round(pflops / (ms * 1e-3) / 1e12, 1),
                         "mfma_frac": round(pflops / (ms * 1e-3) / PEAK_BF16, 4),
                         "tok_per_s": round(pw.T / (ms * 1e-3), 1),
-                        "kernels": {kname: round(v[1] / v[0], 5) for kname, v in kp.items()}}
+                        "kernels": kk}
             if plen == 4096 and model == "qwen3-32b":
                 pc = synth.custom_attention(5, nprompt, pw.Hq, pw.Hkv, pw.D, pw.lens).to(dev)
                 aflex.kv_write(pc, pw.k, pw.v, pw.cu_seqlens, max_seqlen=plen)
-                aflex.profile_start(["kv_write"])
-                ms = timed(lambda: aflex.kv_write(pc, pw.k, pw.v, pw.cu_seqlens, max_seqlen=plen), 10)
-                kp = aflex.profile_stop()
+                ms, kk = timed_kernels(lambda: aflex.kv_write(pc, pw.k, pw.v, pw.cu_seqlens, max_seqlen=plen), 10, ["kv_write"], aflex)
                 kvb = 2 * 2 * pw.k.numel() * 2
                 ops[f"kv_write_qwen3_{nprompt}x{plen}"] = {
                     "ms": round(ms, 5), "GB_per_s": round(kvb / (ms * 1e-3) / 1e9, 1),
                     "hbm_frac": round(kvb / (ms * 1e-3) / PEAK_HBM, 4), "bytes": kvb,
-                    "kernels": {kname: round(v[1] / v[0], 5) for kname, v in kp.items()}}
+                    "kernels": kk}
                 del pc
             del pw, outp
         Tp = 4096
@@ -496,26 +492,22 @@ def main():
         xp = synth.prefill_ffn_tokens(5120, Tp, device=dev)
         yp = torch.empty(Tp, 5120, dtype=torch.bfloat16, device=dev)
         aflex.ffn_swiglu(xp, wd, y=yp)
-        aflex.profile_start(["gemm_gate_up", "gemm_down", "splitk_reduce"])
-        ms = timed(lambda: aflex.ffn_swiglu(xp, wd, y=yp), 5)
-        kp = aflex.profile_stop()
+        ms, kk = timed_kernels(lambda: aflex.ffn_swiglu(xp, wd, y=yp), 5, ["gemm_gate_up", "gemm_down", "splitk_reduce"], aflex)
         flops = 6 * Tp * 5120 * 25600
         ops[f"prefill_swiglu_qwen3_T{Tp}"] = {
             "ms": round(ms, 5), "tflops": round(flops / (ms * 1e-3) / 1e12, 1),
             "mfma_frac": round(flops / (ms * 1e-3) / PEAK_BF16, 4), "tok_per_s": round(Tp / (ms * 1e-3), 1),
-            "kernels": {kname: round(v[1] / v[0], 5) for kname, v in kp.items()}}
+            "kernels": kk}
         del wd, xp, yp
         wm = synth.mixtral_moe(device=dev, T=Tp, seed=7, weights=f)
         yp = torch.empty(Tp, H, dtype=torch.bfloat16, device=dev)
         aflex.moe_ffn(wm.x, wm.ffn, wm.router_logits, 2, y=yp)
-        aflex.profile_start(None)
-        ms = timed(lambda: aflex.moe_ffn(wm.x, wm.ffn, wm.router_logits, 2, y=yp), 5)
-        kp = aflex.profile_stop()
+        ms, kk = timed_kernels(lambda: aflex.moe_ffn(wm.x, wm.ffn, wm.router_logits, 2, y=yp), 5, None, aflex)
         flops = Tp * 2 * 6 * H * I
         ops[f"prefill_moe_mixtral_T{Tp}"] = {
             "ms": round(ms, 5), "tflops": round(flops / (ms * 1e-3) / 1e12, 1),
             "mfma_frac": round(flops / (ms * 1e-3) / PEAK_BF16, 4), "tok_per_s": round(Tp / (ms * 1e-3), 1),
-            "kernels": {kname: round(v[1] / v[0], 5) for kname, v in kp.items()}}
+            "kernels": kk}
         del wm, yp
         result["operators"] = ops
 
