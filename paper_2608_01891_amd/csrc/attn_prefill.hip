@@ -8,29 +8,30 @@
 //
 // Work decomposition: one work-group per (query head, prompt, 128-row query
 // tile); its 4 waves own 32 query rows each and walk the prompt's keys in
-// tiles of 64 up to the causal limit of the tile. Query tiles are dispatched
+// tiles of 64 up to the causal limit of their rows. Query tiles are dispatched
 // longest-first (they are the slow index of the grid, reversed) so the short
 // diagonal tiles fill the tail. When Hq is a multiple of 8 the head index is
 // permuted so that the heads sharing one KV head run on the same XCD and
 // share its L2.
 //
-// Per 64-key tile and wave (v_mfma_f32_32x32x16_bf16 throughout):
-//   S^T = K Q^T   two 32-key blocks x 8 k-steps of d; the query fragments
-//                 (B operand) stay in registers for the whole kernel, K (A
-//                 operand) is read from an LDS tile filled by direct
-//                 global->LDS loads (double buffered, 16-byte chunks XOR
-//                 swizzled by row so fragment reads are conflict-free).
-//   softmax       online, in the log2 domain: each lane holds 32 scores of
-//                 one query row (the accumulator's column), the other 32 sit
-//                 in lane l ^ 32; O and l are rescaled only when a row's
-//                 maximum rises more than 2^8 above the reference maximum.
+// K and V tiles (64 keys x 128 d, row-major, 16-byte chunks XOR-swizzled by
+// row so that both kinds of fragment read are free of bank conflicts) stream from HBM straight into double-buffered LDS (direct global->LDS
+// loads); K runs one tile ahead of V. Per 64-key tile and wave, all products
+// on v_mfma_f32_32x32x16_bf16:
+//   S^T = K Q^T     two 32-key blocks x 8 k-steps of d; the query fragments
+//                   (B operand) stay in registers for the whole kernel.
+//   softmax         online, in the log2 domain: each lane holds 32 scores of
+//                   one query row (an accumulator column), the other 32 sit in
+//                   lane l ^ 32; O and l are rescaled only when a row's maximum
+//                   rises more than 2^8 above the reference maximum.
 //   O^T += V^T P^T  P^T is used straight from the S^T accumulator registers as
-//                 the B operand (rounded to bf16), which fixes the order of the
-//                 keys inside each 16-key k-step; V is transposed in registers
-//                 (v_perm) while it is staged, into an LDS tile [d][key'] whose
-//                 key order matches, so each A fragment is one 16-byte read.
-// The output tile is transposed back through LDS and written with 16-byte
-// row-contiguous stores.
+//                   the B operand (rounded to bf16); the V^T fragments (A
+//                   operand) come from the row-major V tile through the
+//                   transposing LDS read (ds_read_b64_tr_b16), in the key order
+//                   the accumulator layout fixes.
+// The scores of tile kt+1 are multiplied while the softmax of tile kt runs, so
+// the MFMA and vector pipes of a wave overlap. The output tile is transposed
+// back through LDS and written with 16-byte row-contiguous stores.
 #include "common.h"
 #include "gemm.h"
 #include "kernels.h"
@@ -43,6 +44,7 @@ namespace {
 constexpr int kPM = 128;  // query rows per work-group
 constexpr int kPN = 64;   // keys per tile
 constexpr int kPD = 128;  // head dimension
+constexpr int kTile = kPN * kPD * 2;  // bytes of one K or V tile
 
 struct PrefillParams {
   const uint16_t* q;
@@ -55,21 +57,27 @@ struct PrefillParams {
 };
 
 typedef float f32x8 __attribute__((ext_vector_type(8)));
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef short s16x8 __attribute__((ext_vector_type(8)));
 
-__device__ __forceinline__ void wait_vm8() { asm volatile("s_waitcnt vmcnt(8)" ::: "memory"); }
 __device__ __forceinline__ void wait_vm0() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
-// Byte offset of 16-byte chunk `chunk` of row `row` in the K tile (256-byte
-// rows, one 64-bank window each): 16 consecutive rows put a given chunk on 16
-// distinct bank groups.
-__device__ __forceinline__ uint32_t k_off(int row, int chunk) { return row * 256 + ((chunk ^ (row & 15)) << 4); }
-// Byte offset of 16-byte chunk `chunk` of row d in the V^T tile (128-byte rows).
-__device__ __forceinline__ uint32_t v_off(int d, int chunk) { return d * 128 + ((chunk ^ ((d + (d >> 3)) & 7)) << 4); }
+// Swizzle of the 16-byte chunks of a K or V tile row (256-byte rows, one
+// 64-bank window each). Two reads must be conflict-free: 16-byte K fragments
+// of 16 consecutive rows (any 16 distinct values do), and transposing reads in
+// which each half-wave takes 64 contiguous bytes of 4 consecutive rows (the
+// rows must land in different 64-byte quarters: bits 2-3 from row % 4).
+__device__ __forceinline__ int kv_swz(int row) { return ((row & 3) << 2) | ((row >> 2) & 3); }
+__device__ __forceinline__ uint32_t kv_off(int row, int chunk) { return row * 256 + ((chunk ^ kv_swz(row)) << 4); }
+
+// Transposing LDS read: within each 16-lane group, lane i receives element
+// i % 4 of the 4-element segment addressed by lane 4 j + i / 4, as element j.
+__device__ __forceinline__ s16x4 lds_read_tr16(const uint8_t* p) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16((s16x4 __attribute__((address_space(3)))*)p);
+}
 
 __global__ __launch_bounds__(256, 2) void attn_prefill_kernel(PrefillParams p) {
-  __shared__ __attribute__((aligned(16))) uint8_t smem[2 * kPN * kPD * 2 + 2 * kPD * kPN * 2];
-  uint8_t* const ksm = smem;                         // 2 x 16 KiB K tiles [key][d]
-  uint8_t* const vsm = smem + 2 * kPN * kPD * 2;     // 2 x 16 KiB V^T tiles [d][key']
+  __shared__ __attribute__((aligned(16))) uint8_t smem[4 * kTile];  // K0, K1, V0, V1
 
   int h = blockIdx.x;
   if ((p.Hq & 7) == 0) h = (h & 7) * (p.Hq >> 3) + (h >> 3);
@@ -96,65 +104,49 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_kernel(PrefillParams p) {
     for (int ks = 0; ks < kPD / 16; ++ks) qf[ks] = ld_bf16x8(qrow + ks * 16);
   }
 
-  const int kend = min(n, q0 + kPM);
-  const int nkt = (kend + kPN - 1) / kPN;
+  const int nkt = (min(n, q0 + kPM) + kPN - 1) / kPN;                // tiles the work-group stages
+  const int wkt = qr0 < n ? min(nkt, min(qr0 + 31, n - 1) / kPN + 1) : 0;  // tiles this wave multiplies
   const uint16_t* kbase = p.k + (size_t)s0 * kvstride + (size_t)g * kPD;
   const uint16_t* vbase = p.v + (size_t)s0 * kvstride + (size_t)g * kPD;
-  const uint32_t ksm_lds = lds_offset(ksm);
+  const uint32_t lds0 = lds_offset(smem);
 
-  // K staging: wave-load i of thread tid fills slot i * 256 + tid, i.e. row
-  // i * 16 + tid / 16 and stored chunk tid % 16 of the tile; the logical chunk
-  // is the same for all four wave-loads of a thread.
-  const int krow = tid >> 4, kchunk = (tid & 15) ^ krow;
-  const uint16_t* kp = kbase + (size_t)krow * kvstride + kchunk * 8;
-  auto issue_k = [&](int kt, int buf) {
-    const uint32_t lds = ksm_lds + buf * 16384 + w * 1024;
+  // Staging: wave-load i of thread tid fills slot i * 256 + tid of the tile,
+  // i.e. row i * 16 + tid / 16 and stored chunk tid % 16; the logical chunk is
+  // the same for all four wave-loads of a thread.
+  const int srow = tid >> 4, schunk = (tid & 15) ^ kv_swz(srow);
+  const size_t soff = (size_t)srow * kvstride + schunk * 8;
+  auto issue = [&](const uint16_t* base, int kt, uint32_t lds) {
+    lds += w * 1024;
     if (kt * kPN + kPN <= n) {
 #pragma unroll
-      for (int i = 0; i < 4; ++i) lds_dma16(kp + (size_t)(kt * kPN + i * 16) * kvstride, lds + i * 4096);
-    } else {  // tail tile: rows past the prompt re-read its last row (their scores are masked)
+      for (int i = 0; i < 4; ++i) lds_dma16(base + soff + (size_t)(kt * kPN + i * 16) * kvstride, lds + i * 4096);
+    } else {  // tail tile: rows past the prompt re-read its last row (masked / weighted 0)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const int key = min(kt * kPN + i * 16 + krow, n - 1);
-        lds_dma16(kbase + (size_t)key * kvstride + kchunk * 8, lds + i * 4096);
+        const int key = min(kt * kPN + i * 16 + srow, n - 1);
+        lds_dma16(base + (size_t)key * kvstride + schunk * 8, lds + i * 4096);
       }
     }
   };
-  // V staging: thread tid loads keys 4a .. 4a+3 (a = tid / 16) at d = 8 (tid % 16) + [0, 8).
-  const int va = tid >> 4, vdc = tid & 15;
-  const uint16_t* vp = vbase + (size_t)(va * 4) * kvstride + vdc * 8;
-  uint4 vr[4];
-  auto load_v = [&](int kt) {
-    if (kt * kPN + kPN <= n) {
+
+  // Per-lane LDS byte offsets inside a tile. K fragment of k-step ks: row lr
+  // (+32 for the second key block), chunk 2 ks + hi. Transposing V read of
+  // d-block db: the lane addresses the 8-byte segment of row hi*4 + (l%16)/4
+  // (+16 ks, +8 for the upper four keys) at d = 32 db + 16 ((l/16)%2) + 4 (l%4).
+  // (Rows 32 and 16 further down share the swizzle, so those are immediates;
+  // the upper four keys (+8 rows) do not, hence two transposing bases.)
+  uint32_t k_off[kPD / 16], tr_lo[kPD / 32], tr_up[kPD / 32];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) vr[j] = *reinterpret_cast<const uint4*>(vp + (size_t)(kt * kPN + j) * kvstride);
-    } else {  // tail tile: rows past the prompt re-read its last row (their weights are 0)
+  for (int ks = 0; ks < kPD / 16; ++ks) k_off[ks] = kv_off(lr, ks * 2 + hi);
+  {
+    const int tr_row = hi * 4 + ((l & 15) >> 2);
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int key = min(kt * kPN + va * 4 + j, n - 1);
-        vr[j] = *reinterpret_cast<const uint4*>(vbase + (size_t)key * kvstride + vdc * 8);
-      }
+    for (int db = 0; db < kPD / 32; ++db) {
+      const int ch = db * 4 + ((l >> 4) & 1) * 2 + ((l & 3) >> 1);
+      tr_lo[db] = kv_off(tr_row, ch) + (l & 1) * 8;
+      tr_up[db] = kv_off(tr_row + 8, ch) + (l & 1) * 8;
     }
-  };
-  // Keys 4a' .. 4a'+3 of a 16-key group sit at positions (a' % 2) * 8 + (a' / 2) * 4 + [0, 4)
-  // of that group in the V^T tile: the order in which the S^T accumulator holds them.
-  auto store_vt = [&](int buf) {
-    const int grp = va >> 2, ap = va & 3;
-    const int chunk = grp * 2 + (ap & 1), within = (ap >> 1) * 8;
-    const uint32_t w0[4] = {vr[0].x, vr[0].y, vr[0].z, vr[0].w};
-    const uint32_t w1[4] = {vr[1].x, vr[1].y, vr[1].z, vr[1].w};
-    const uint32_t w2[4] = {vr[2].x, vr[2].y, vr[2].z, vr[2].w};
-    const uint32_t w3[4] = {vr[3].x, vr[3].y, vr[3].z, vr[3].w};
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const uint32_t sel = (e & 1) ? 0x07060302u : 0x05040100u;
-      uint2 val;
-      val.x = __builtin_amdgcn_perm(w1[e >> 1], w0[e >> 1], sel);
-      val.y = __builtin_amdgcn_perm(w3[e >> 1], w2[e >> 1], sel);
-      const int d = vdc * 8 + e;
-      *reinterpret_cast<uint2*>(vsm + buf * 16384 + v_off(d, chunk) + within) = val;
-    }
-  };
+  }
 
   f32x16 oacc[kPD / 32];
 #pragma unroll
@@ -162,99 +154,102 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_kernel(PrefillParams p) {
 #pragma unroll
     for (int i = 0; i < 16; ++i) oacc[db][i] = 0.f;
   float m_run = kNegInf, l_run = 0.f;
+  f32x16 sc0, sc1, sn0, sn1;  // scores of the current tile and of the next one
 
-  issue_k(0, 0);
-  load_v(0);
-  for (int kt = 0; kt < nkt; ++kt) {
-    const int buf = kt & 1;
-    if (kt > 0) __syncthreads();  // every wave is done with tile kt - 1
-    store_vt(buf);
-    if (kt + 1 < nkt) {
-      issue_k(kt + 1, buf ^ 1);
-      load_v(kt + 1);
-      wait_vm8();  // this thread's part of K tile kt has landed
-    } else {
-      wait_vm0();
-    }
-    __syncthreads();
+#define AFLEX_QK(S0, S1, BUF)                                                                    \
+  do {                                                                                           \
+    _Pragma("unroll") for (int i = 0; i < 16; ++i) { S0[i] = 0.f; S1[i] = 0.f; }                 \
+    const uint8_t* kl_ = smem + (BUF) * kTile;                                                   \
+    _Pragma("unroll") for (int ks = 0; ks < kPD / 16; ++ks) {                                    \
+      const bf16x8 a0_ = *reinterpret_cast<const bf16x8*>(kl_ + k_off[ks]);                      \
+      const bf16x8 a1_ = *reinterpret_cast<const bf16x8*>(kl_ + k_off[ks] + 32 * 256);           \
+      S0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0_, qf[ks], S0, 0, 0, 0);                    \
+      S1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1_, qf[ks], S1, 0, 0, 0);                    \
+    }                                                                                            \
+  } while (0)
 
-    const int kb0 = kt * kPN;
-    if (kb0 > qr0 + 31 || qr0 >= n) continue;  // every key of the tile is masked for this wave
+  // One key tile. KT is the tile, PAR = KT % 2 (a compile-time constant, so
+  // every LDS address is a per-lane base plus an immediate), MASK whether any
+  // key of the tile can lie past a row of the work-group or past the prompt.
+  // SC0/SC1 hold the tile's scores on entry; SN0/SN1 receive the next tile's.
+#define AFLEX_TILE(KT, PAR, MASK, SC0, SC1, SN0, SN1)                                         \
+  do {                                                                                       \
+    wait_vm0();                                                                              \
+    __syncthreads();                                                                         \
+    if ((KT) + 2 < nkt) issue(kbase, (KT) + 2, lds0 + (PAR) * kTile);                          \
+    if ((KT) + 1 < nkt) issue(vbase, (KT) + 1, lds0 + (3 - (PAR)) * kTile);                    \
+    if ((KT) < wkt) {                                                                        \
+      if (MASK) {                                                                            \
+        const int lim_ = min(qi, n - 1), kb0_ = (KT) * kPN;                                  \
+        _Pragma("unroll") for (int i = 0; i < 16; ++i) {                                     \
+          const int key_ = kb0_ + (i >> 2) * 8 + hi * 4 + (i & 3);                           \
+          if (key_ > lim_) SC0[i] = kNegInf;                                                 \
+          if (key_ + 32 > lim_) SC1[i] = kNegInf;                                            \
+        }                                                                                    \
+      }                                                                                      \
+      float mx_ = kNegInf;                                                                   \
+      _Pragma("unroll") for (int i = 0; i < 16; ++i) mx_ = fmaxf(mx_, fmaxf(SC0[i], SC1[i])); \
+      mx_ = fmaxf(mx_, __shfl_xor(mx_, 32));                                                 \
+      if (__ballot((mx_ - m_run) * p.c > 8.f) != 0) {                                        \
+        const float mnew_ = fmaxf(m_run, mx_);                                               \
+        const float alpha_ = fast_exp2((m_run - mnew_) * p.c);                               \
+        l_run *= alpha_;                                                                     \
+        _Pragma("unroll") for (int db = 0; db < kPD / 32; ++db)                              \
+            _Pragma("unroll") for (int i = 0; i < 16; ++i) oacc[db][i] *= alpha_;            \
+        m_run = mnew_;                                                                       \
+      }                                                                                      \
+      /* next tile's scores: independent of the exponentials below, which the */             \
+      /* scheduler interleaves with them (dropped after a wave's last tile)   */             \
+      AFLEX_QK(SN0, SN1, 1 - (PAR));                                                         \
+      const float mc_ = m_run * p.c;                                                         \
+      float lsum_ = 0.f;                                                                     \
+      bf16x8 pb_[4];                                                                         \
+      _Pragma("unroll") for (int ks = 0; ks < 4; ++ks) {                                     \
+        f32x8 pv_;                                                                           \
+        _Pragma("unroll") for (int e = 0; e < 8; ++e) {                                      \
+          const float s_ = (ks < 2) ? SC0[(ks & 1) * 8 + e] : SC1[(ks & 1) * 8 + e];         \
+          const float pe_ = fast_exp2(__builtin_fmaf(s_, p.c, -mc_));                        \
+          lsum_ += pe_;                                                                      \
+          pv_[e] = pe_;                                                                      \
+        }                                                                                    \
+        pb_[ks] = __builtin_convertvector(pv_, bf16x8);                                      \
+      }                                                                                      \
+      l_run += lsum_;                                                                        \
+      /* O^T += V^T P^T: slot hi*8 + e of k-step ks is key ks*16 + (e/4)*8 + hi*4 + e%4 */    \
+      const uint8_t* vl_ = smem + (2 + (PAR)) * kTile;                                       \
+      _Pragma("unroll") for (int ks = 0; ks < 4; ++ks) {                                     \
+        _Pragma("unroll") for (int db = 0; db < kPD / 32; ++db) {                            \
+          const s16x4 lo_ = lds_read_tr16(vl_ + tr_lo[db] + ks * 4096);                      \
+          const s16x4 up_ = lds_read_tr16(vl_ + tr_up[db] + ks * 4096);                      \
+          const bf16x8 a_ = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo_, up_, 0, 1, 2, 3, 4, 5, 6, 7)); \
+          oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a_, pb_[ks], oacc[db], 0, 0, 0);  \
+        }                                                                                    \
+      }                                                                                      \
+    }                                                                                        \
+  } while (0)
 
-    // S^T = K Q^T
-    f32x16 sacc[2];
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int i = 0; i < 16; ++i) sacc[kb][i] = 0.f;
-    const uint8_t* kt_lds = ksm + buf * 16384;
-#pragma unroll
-    for (int ks = 0; ks < kPD / 16; ++ks) {
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {
-        const bf16x8 a = *reinterpret_cast<const bf16x8*>(kt_lds + k_off(kb * 32 + lr, ks * 2 + hi));
-        sacc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[ks], sacc[kb], 0, 0, 0);
-      }
-    }
+  // Prologue: K(0), V(0), K(1) resident, S(0) computed.
+  issue(kbase, 0, lds0);
+  issue(vbase, 0, lds0 + 2 * kTile);
+  if (nkt > 1) issue(kbase, 1, lds0 + kTile);
+  wait_vm0();
+  __syncthreads();
+  if (wkt > 0) AFLEX_QK(sc0, sc1, 0);
 
-    // Mask keys past the query row or past the prompt (diagonal and tail tiles only).
-    if (kb0 + kPN - 1 > qr0 || kb0 + kPN > n) {
-      const int lim = min(qi, n - 1);
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          const int key = kb0 + kb * 32 + (i >> 2) * 8 + hi * 4 + (i & 3);
-          if (key > lim) sacc[kb][i] = kNegInf;
-        }
-    }
-
-    float mx = kNegInf;
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int i = 0; i < 16; ++i) mx = fmaxf(mx, sacc[kb][i]);
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
-    // The reference maximum m_run only moves when a row's scores exceed it by
-    // more than 2^8 in the exponent: O and l share the reference, so the
-    // normalised result does not depend on it, and the weights stay <= 256.
-    if (__ballot((mx - m_run) * p.c > 8.f) != 0) {
-      const float mnew = fmaxf(m_run, mx);
-      const float alpha = fast_exp2((m_run - mnew) * p.c);
-      l_run *= alpha;
-#pragma unroll
-      for (int db = 0; db < kPD / 32; ++db)
-#pragma unroll
-        for (int i = 0; i < 16; ++i) oacc[db][i] *= alpha;
-      m_run = mnew;
-    }
-    const float mc = m_run * p.c;
-    float lsum = 0.f;
-    bf16x8 pb[4];
-#pragma unroll
-    for (int ks = 0; ks < 4; ++ks) {
-      f32x8 pv;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const float pe = fast_exp2(__builtin_fmaf(sacc[ks >> 1][(ks & 1) * 8 + e], p.c, -mc));
-        lsum += pe;
-        pv[e] = pe;
-      }
-      pb[ks] = __builtin_convertvector(pv, bf16x8);
-    }
-    l_run += lsum;
-
-    // O^T += V^T P^T
-    const uint8_t* vt_lds = vsm + buf * 16384;
-#pragma unroll
-    for (int ks = 0; ks < 4; ++ks) {
-#pragma unroll
-      for (int db = 0; db < kPD / 32; ++db) {
-        const bf16x8 a = *reinterpret_cast<const bf16x8*>(vt_lds + v_off(db * 32 + lr, ks * 2 + hi));
-        oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[ks], oacc[db], 0, 0, 0);
-      }
-    }
+  // Tiles below every row of the work-group and inside the prompt need no
+  // mask; an even count keeps the two register sets and buffers in step.
+  const int kfull = min(q0 / kPN, n / kPN) & ~1;
+  int kt = 0;
+  for (; kt < kfull; kt += 2) {
+    AFLEX_TILE(kt, 0, false, sc0, sc1, sn0, sn1);
+    AFLEX_TILE(kt + 1, 1, false, sn0, sn1, sc0, sc1);
   }
+  for (; kt < nkt; kt += 2) {
+    AFLEX_TILE(kt, 0, true, sc0, sc1, sn0, sn1);
+    if (kt + 1 < nkt) AFLEX_TILE(kt + 1, 1, true, sn0, sn1, sc0, sc1);
+  }
+#undef AFLEX_TILE
+#undef AFLEX_QK
 
   // Normalise and write: each wave transposes its 32 x 128 tile through its
   // own 8 KiB of LDS (chunk c of row r stored at chunk c ^ (r % 16)).
