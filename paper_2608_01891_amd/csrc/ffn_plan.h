@@ -12,7 +12,7 @@ inline int gate_bn(int bm) { return bm >= 256 ? 128 : 64; }
 inline int down_bn(int) { return 128; }
 // Work-groups the down GEMM's split-K aims for: the 256-row tiles run one
 // work-group per CU, so one round of the chip; smaller tiles two per CU.
-inline int down_target(int bm) { return bm >= 256 ? 256 : 512; }
+inline int down_target(int bm) { return bm >= 256 ? 256 : (bm == 64 ? 2048 : (bm == 128 ? 1024 : 512)); }
 
 struct FfnPlan {
   int bm;           // rows per m-tile: 32, 64 or 128

@@ -12,6 +12,7 @@
 // speed.
 //
 // Variants (template flags):
+//   NT_B    weight (B) tile loads are non-temporal.
 //   DUAL    two weight matrices (gate, up) share the A tile; the epilogue
 //           applies SiLU(gate) * up and stores bf16 (the fused SwiGLU step).
 //   OUT_F32 store the fp32 accumulator into split-K partials (one slice per
@@ -79,6 +80,22 @@ __device__ __forceinline__ void lds_dma16(const void* gptr, uint32_t lds) {
       : "memory");
 }
 
+// The same load marked non-temporal: weights that one work-group streams
+// exactly once (a 32-row tile covers all of a decode microbatch's rows of an
+// expert) need not stay in the caches.
+__device__ __forceinline__ void lds_dma16_nt(const void* gptr, uint32_t lds) {
+  const uint32_t lds_s = __builtin_amdgcn_readfirstlane(lds);
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %2\n\t"
+      "global_load_lds_dwordx4 %1, off nt\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "v"(gptr), "s"(lds_s)
+      : "memory");
+}
+
 __device__ __forceinline__ int xcd_remap(int w, int nwg) {
   const int q = nwg >> 3, rem = nwg & 7, x = w & 7, j = w >> 3;
   return (x < rem ? x * (q + 1) : rem * (q + 1) + (x - rem) * q) + j;
@@ -89,7 +106,7 @@ __device__ __forceinline__ int xcd_remap(int w, int nwg) {
 // BK-wide k-steps, LDS_BYTES of LDS per work-group (the ring has as many
 // stages as fit; 80 KiB lets two work-groups share a CU). The 32x32 MFMA
 // sustains a higher issue rate and serves the MFMA-bound tiles.
-template <int BM, int BN, int WM, int WN, int BK, int MS, bool DUAL, bool OUT_F32, int LDS_BYTES>
+template <int BM, int BN, int WM, int WN, int BK, int MS, bool DUAL, bool OUT_F32, int LDS_BYTES, bool NT_B = false>
 __global__ __launch_bounds__(64 * WM * WN, LDS_BYTES > 81920 ? 1 : 2) void gemm_nt_kernel(GemmParams p) {
   constexpr int NW = WM * WN;
   constexpr int NB = DUAL ? 2 : 1;
@@ -175,7 +192,10 @@ __global__ __launch_bounds__(64 * WM * WN, LDS_BYTES > 81920 ? 1 : 2) void gemm_
   do {                                                                                   \
     const int ko_ = min(KT, nk - 1) * BK;                                                \
     _Pragma("unroll") for (int j = 0; j < IPW; ++j)                                      \
-        lds_dma16(src[j] + ko_, lds_offset(SM + (wave + NW * j) * 512));                 \
+        if (NT_B && ((wave + NW * j) * 64) / CPR >= BM)                                    \
+          lds_dma16_nt(src[j] + ko_, lds_offset(SM + (wave + NW * j) * 512));              \
+        else                                                                             \
+          lds_dma16(src[j] + ko_, lds_offset(SM + (wave + NW * j) * 512));                 \
   } while (0)
 
   Acc acc[NB][TM][TN];

@@ -1,7 +1,8 @@
 // Instantiations of the FFN GEMM tiles and their launch helpers.
 //
 // Row-tile size selects the shape: up to 128 token rows the GEMMs stream
-// weights (4 waves, 16x16x32 MFMA, 64-wide k-steps, HBM-bound); 256-row tiles
+// weights (4 waves, 16x16x32 MFMA, 64-wide k-steps, HBM-bound; the 32-row
+// tiles, which read each weight once, load them non-temporally); 256-row tiles
 // are the MFMA-bound shape (8 waves with 128 x 64 (gate/up) or 64 x 64 (down)
 // wave tiles of 32x32x16 MFMAs, 32-wide k-steps, a ring of five or six stages
 // in the whole 160 KiB of LDS, one work-group per CU).
@@ -10,9 +11,9 @@
 
 namespace aflex {
 
-template <int BM, int BN, int WM, int WN, int BK, int MS, bool DUAL, bool F32, int LDS>
+template <int BM, int BN, int WM, int WN, int BK, int MS, bool DUAL, bool F32, int LDS, bool NT = false>
 static void go(const GemmParams& g, unsigned grid, hipStream_t stream) {
-  gemm_nt_kernel<BM, BN, WM, WN, BK, MS, DUAL, F32, LDS><<<grid, 64 * WM * WN, 0, stream>>>(g);
+  gemm_nt_kernel<BM, BN, WM, WN, BK, MS, DUAL, F32, LDS, NT><<<grid, 64 * WM * WN, 0, stream>>>(g);
 }
 
 static unsigned grid_of(const GemmParams& g) {
@@ -24,7 +25,7 @@ hipError_t launch_gate_up(int bm, const GemmParams& g, hipStream_t stream) {
   if (grid == 0) return hipSuccess;
   ProfScope ps("gemm_gate_up", stream);
   switch (bm) {
-    case 32: go<32, 64, 1, 4, 64, 16, true, false, 81920>(g, grid, stream); break;
+    case 32: go<32, 64, 1, 4, 64, 16, true, false, 81920, true>(g, grid, stream); break;
     case 64: go<64, 64, 2, 2, 64, 16, true, false, 81920>(g, grid, stream); break;
     case 128: go<128, 64, 2, 2, 64, 16, true, false, 163840>(g, grid, stream); break;
     default: go<256, 128, 2, 4, 32, 32, true, false, 163840>(g, grid, stream); break;
@@ -35,7 +36,7 @@ hipError_t launch_gate_up(int bm, const GemmParams& g, hipStream_t stream) {
 template <bool F32>
 static void down(int bm, const GemmParams& g, unsigned grid, hipStream_t stream) {
   switch (bm) {
-    case 32: go<32, 128, 1, 4, 64, 16, false, F32, 81920>(g, grid, stream); break;
+    case 32: go<32, 128, 1, 4, 64, 16, false, F32, 81920, true>(g, grid, stream); break;
     case 64: go<64, 128, 2, 2, 64, 16, false, F32, 81920>(g, grid, stream); break;
     case 128: go<128, 128, 2, 2, 64, 16, false, F32, 163840>(g, grid, stream); break;
     default: go<256, 128, 4, 2, 32, 32, false, F32, 163840>(g, grid, stream); break;
