@@ -9,10 +9,11 @@ namespace aflex {
 // Output columns per gate/up tile (x2 weight rows) and per down tile.
 inline int gate_bn(int bm) { return bm >= 256 ? 128 : 64; }
 
-inline int down_bn(int) { return 128; }
+inline int down_bn(int bm) { return bm >= 256 ? 256 : 128; }
 // Work-groups the down GEMM's split-K aims for: the 256-row tiles run one
 // work-group per CU, so one round of the chip; smaller tiles two per CU.
-inline int down_target(int bm) { return bm >= 256 ? 256 : (bm == 64 ? 2048 : (bm == 128 ? 1024 : 512)); }
+constexpr int kOneWgPerCuTarget = 256;
+inline int down_target(int bm) { return bm >= 256 ? kOneWgPerCuTarget : (bm == 64 ? 2048 : (bm == 128 ? 1024 : 512)); }
 
 struct FfnPlan {
   int bm;           // rows per m-tile: 32, 64 or 128
@@ -31,12 +32,31 @@ inline int pick_bm(double rows_per_expert) {
 }
 
 // Split K so that the down GEMM has about `target` work-groups, keeping at
-// least `min_steps` 64-wide k-steps per split.
+// least `min_steps` 64-wide k-steps per split. The 256-row tiles run one
+// work-group per CU, so for them the split count is the smallest that fills
+// the rounds of 256 CUs it needs to at least 90% (measured best for the dense
+// down GEMM at T = 256 ... 4096: 12, 6, 3, 3-4 splits); more splits only add
+// fp32 partials to reduce.
 inline void plan_splits(int base_tiles, int K, int target, int min_steps, int* splits, int* kps) {
   const int ksteps = K / 64;
-  int s = (target + base_tiles - 1) / base_tiles;
   int smax = ksteps / min_steps;
   if (smax < 1) smax = 1;
+  int s = (target + base_tiles - 1) / base_tiles;
+  if (target == kOneWgPerCuTarget) {
+    double best_u = 0.0;
+    for (int c = 1; c <= smax && c <= 64; ++c) {
+      const long long wgs = (long long)base_tiles * c;
+      const double u = (double)wgs / (double)(((wgs + 255) / 256) * 256);
+      if (u >= 0.9) {
+        s = c;
+        break;
+      }
+      if (u > best_u + 1e-9) {
+        best_u = u;
+        s = c;
+      }
+    }
+  }
   if (s > smax) s = smax;
   if (s < 1) s = 1;
   const int steps = (ksteps + s - 1) / s;

@@ -3,8 +3,8 @@
 // Row-tile size selects the shape: up to 128 token rows the GEMMs stream
 // weights (4 waves, 16x16x32 MFMA, 64-wide k-steps, HBM-bound; the 32-row
 // tiles, which read each weight once, load them non-temporally); 256-row tiles
-// are the MFMA-bound shape (8 waves with 128 x 64 (gate/up) or 64 x 64 (down)
-// wave tiles of 32x32x16 MFMAs, 32-wide k-steps, a ring of five or six stages
+// are the MFMA-bound shape (8 waves with 128 x 64 wave tiles (gate/up: 128
+// x 32 of each weight matrix) of 32x32x16 MFMAs, 32-wide k-steps, a ring of five or six stages
 // in the whole 160 KiB of LDS, one work-group per CU).
 #include "ffn_plan.h"
 #include "profile.h"
@@ -39,7 +39,7 @@ static void down(int bm, const GemmParams& g, unsigned grid, hipStream_t stream)
     case 32: go<32, 128, 1, 4, 64, 16, false, F32, 81920, true>(g, grid, stream); break;
     case 64: go<64, 128, 2, 2, 64, 16, false, F32, 81920>(g, grid, stream); break;
     case 128: go<128, 128, 2, 2, 64, 16, false, F32, 163840>(g, grid, stream); break;
-    default: go<256, 128, 4, 2, 32, 32, false, F32, 163840>(g, grid, stream); break;
+    default: go<256, 256, 2, 4, 32, 32, false, F32, 163840>(g, grid, stream); break;
   }
 }
 
