@@ -13,21 +13,22 @@ inline int down_bn(int bm) { return bm >= 256 ? 256 : 128; }
 // Work-groups the down GEMM's split-K aims for: the 256-row tiles run one
 // work-group per CU, so one round of the chip; smaller tiles two per CU.
 constexpr int kOneWgPerCuTarget = 256;
-inline int down_target(int bm) { return bm >= 256 ? kOneWgPerCuTarget : (bm == 64 ? 2048 : (bm == 128 ? 1024 : 512)); }
+inline int down_target(int bm) { return bm >= 256 ? kOneWgPerCuTarget : (bm == 64 ? 2048 : 512); }
 
 struct FfnPlan {
-  int bm;           // rows per m-tile: 32, 64 or 128
+  int bm;           // rows per m-tile: 32, 64 or 256
   int down_splits;  // split-K factor of the down GEMM
   int down_kps;     // k elements per split (multiple of 64)
 };
 
-// Rows per m-tile for grouped GEMMs with the given average rows per expert:
-// large enough that a typical expert needs one tile (its weights are then
-// streamed once), up to the MFMA-bound 256-row shape.
+// Rows per m-tile for grouped GEMMs with the given average rows per expert.
+// Up to 32 rows a tile covers a typical expert (its weights are streamed once,
+// non-temporally); up to 160 rows 64-row tiles, two work-groups per CU (an
+// expert's second and third tiles re-read its weights from L2; measured
+// faster than one 128-row tile per CU); beyond, the MFMA-bound 256-row shape.
 inline int pick_bm(double rows_per_expert) {
   if (rows_per_expert * 1.3 <= 32) return 32;
-  if (rows_per_expert <= 72) return 64;
-  if (rows_per_expert <= 160) return 128;
+  if (rows_per_expert <= 160) return 64;
   return 256;
 }
 
@@ -66,7 +67,7 @@ inline void plan_splits(int base_tiles, int K, int target, int min_steps, int* s
 
 inline FfnPlan plan_dense(int T, int H, int I) {
   FfnPlan pl;
-  pl.bm = T <= 32 ? 32 : (T <= 64 ? 64 : (T <= 128 ? 128 : 256));
+  pl.bm = T <= 32 ? 32 : (T <= 64 ? 64 : 256);
   const int mtiles = (T + pl.bm - 1) / pl.bm;
   const int ntiles = (H + down_bn(pl.bm) - 1) / down_bn(pl.bm);
   plan_splits(mtiles * ntiles, I, down_target(pl.bm), 8, &pl.down_splits, &pl.down_kps);

@@ -1,11 +1,12 @@
 // Instantiations of the FFN GEMM tiles and their launch helpers.
 //
-// Row-tile size selects the shape: up to 128 token rows the GEMMs stream
-// weights (4 waves, 16x16x32 MFMA, 64-wide k-steps, HBM-bound; the 32-row
-// tiles, which read each weight once, load them non-temporally); 256-row tiles
-// are the MFMA-bound shape (8 waves with 128 x 64 wave tiles (gate/up: 128
-// x 32 of each weight matrix) of 32x32x16 MFMAs, 32-wide k-steps, a ring of five or six stages
-// in the whole 160 KiB of LDS, one work-group per CU).
+// Row-tile size selects the shape: 32- and 64-row tiles stream weights (4
+// waves, 16x16x32 MFMA, 64-wide k-steps, two work-groups per CU, HBM-bound;
+// the 32-row tiles, which read each weight once, load them non-temporally);
+// 256-row tiles are the MFMA-bound shape (8 waves with 128 x 64 wave tiles
+// (gate/up: 128 x 32 of each weight matrix) of 32x32x16 MFMAs, 32-wide
+// k-steps, a ring of five stages in the whole 160 KiB of LDS, one work-group
+// per CU).
 #include "ffn_plan.h"
 #include "profile.h"
 
@@ -27,7 +28,6 @@ hipError_t launch_gate_up(int bm, const GemmParams& g, hipStream_t stream) {
   switch (bm) {
     case 32: go<32, 64, 1, 4, 64, 16, true, false, 81920, true>(g, grid, stream); break;
     case 64: go<64, 64, 2, 2, 64, 16, true, false, 81920>(g, grid, stream); break;
-    case 128: go<128, 64, 2, 2, 64, 16, true, false, 163840>(g, grid, stream); break;
     default: go<256, 128, 2, 4, 32, 32, true, false, 163840>(g, grid, stream); break;
   }
   return hipGetLastError();
@@ -38,7 +38,6 @@ static void down(int bm, const GemmParams& g, unsigned grid, hipStream_t stream)
   switch (bm) {
     case 32: go<32, 128, 1, 4, 64, 16, false, F32, 81920, true>(g, grid, stream); break;
     case 64: go<64, 128, 2, 2, 64, 16, false, F32, 81920>(g, grid, stream); break;
-    case 128: go<128, 128, 2, 2, 64, 16, false, F32, 163840>(g, grid, stream); break;
     default: go<256, 256, 2, 4, 32, 32, false, F32, 163840>(g, grid, stream); break;
   }
 }
