@@ -59,7 +59,8 @@ hipError_t launch_swiglu(const aflex_ffn_args& f, void* ws, hipStream_t stream) 
   g.mt_major = 0;
   g.C = h;
   g.ldc = f.I;
-  hipError_t e = launch_gate_up(pl.bm, g, stream);
+  const bool once = f.T <= pl.bm;
+  hipError_t e = launch_gate_up(pl.bm, once, g, stream);
   if (e != hipSuccess) return e;
 
   GemmParams d = {};
@@ -80,7 +81,7 @@ hipError_t launch_swiglu(const aflex_ffn_args& f, void* ws, hipStream_t stream) 
   d.P = P;
   d.p_split_stride = (long long)f.T * f.H;
   d.ldp = f.H;
-  e = launch_down(pl.bm, pl.down_splits > 1, d, stream);
+  e = launch_down(pl.bm, pl.down_splits > 1, once, d, stream);
   if (e != hipSuccess || pl.down_splits == 1) return e;
   const long long n4 = (long long)f.T * f.H / 4;
   ProfScope ps("splitk_reduce", stream);
@@ -117,7 +118,7 @@ hipError_t launch_linear(const aflex_linear_args& l, void* ws, hipStream_t strea
   d.P = P;
   d.p_split_stride = (long long)l.T * l.N;
   d.ldp = l.N;
-  hipError_t e = launch_down(pl.bm, pl.down_splits > 1, d, stream);
+  hipError_t e = launch_down(pl.bm, pl.down_splits > 1, l.T <= pl.bm, d, stream);
   if (e != hipSuccess || pl.down_splits == 1) return e;
   const long long n4 = (long long)l.T * l.N / 4;
   ProfScope ps("splitk_reduce", stream);

@@ -2,7 +2,8 @@
 //
 // Row-tile size selects the shape: 32- and 64-row tiles stream weights (4
 // waves, 16x16x32 MFMA, 64-wide k-steps, two work-groups per CU, HBM-bound;
-// the 32-row tiles, which read each weight once, load them non-temporally);
+// weights that one tile streams exactly once load non-temporally: always for
+// 32-row tiles, for 64-row tiles when the caller has a single row tile);
 // 256-row tiles are the MFMA-bound shape (8 waves with 128 x 64 wave tiles
 // (gate/up: 128 x 32 of each weight matrix) of 32x32x16 MFMAs, 32-wide
 // k-steps, a ring of five stages in the whole 160 KiB of LDS, one work-group
@@ -21,35 +22,45 @@ static unsigned grid_of(const GemmParams& g) {
   return (unsigned)((long long)g.max_mtiles * g.n_ntiles * g.splits);
 }
 
-hipError_t launch_gate_up(int bm, const GemmParams& g, hipStream_t stream) {
+hipError_t launch_gate_up(int bm, bool once, const GemmParams& g, hipStream_t stream) {
   const unsigned grid = grid_of(g);
   if (grid == 0) return hipSuccess;
   ProfScope ps("gemm_gate_up", stream);
   switch (bm) {
     case 32: go<32, 64, 1, 4, 64, 16, true, false, 81920, true>(g, grid, stream); break;
-    case 64: go<64, 64, 2, 2, 64, 16, true, false, 81920>(g, grid, stream); break;
+    case 64:
+      if (once)
+        go<64, 64, 2, 2, 64, 16, true, false, 81920, true>(g, grid, stream);
+      else
+        go<64, 64, 2, 2, 64, 16, true, false, 81920>(g, grid, stream);
+      break;
     default: go<256, 128, 2, 4, 32, 32, true, false, 163840>(g, grid, stream); break;
   }
   return hipGetLastError();
 }
 
 template <bool F32>
-static void down(int bm, const GemmParams& g, unsigned grid, hipStream_t stream) {
+static void down(int bm, bool once, const GemmParams& g, unsigned grid, hipStream_t stream) {
   switch (bm) {
     case 32: go<32, 128, 1, 4, 64, 16, false, F32, 81920, true>(g, grid, stream); break;
-    case 64: go<64, 128, 2, 2, 64, 16, false, F32, 81920>(g, grid, stream); break;
+    case 64:
+      if (once)
+        go<64, 128, 2, 2, 64, 16, false, F32, 81920, true>(g, grid, stream);
+      else
+        go<64, 128, 2, 2, 64, 16, false, F32, 81920>(g, grid, stream);
+      break;
     default: go<256, 256, 2, 4, 32, 32, false, F32, 163840>(g, grid, stream); break;
   }
 }
 
-hipError_t launch_down(int bm, bool f32_partials, const GemmParams& g, hipStream_t stream) {
+hipError_t launch_down(int bm, bool f32_partials, bool once, const GemmParams& g, hipStream_t stream) {
   const unsigned grid = grid_of(g);
   if (grid == 0) return hipSuccess;
   ProfScope ps("gemm_down", stream);
   if (f32_partials)
-    down<true>(bm, g, grid, stream);
+    down<true>(bm, once, g, grid, stream);
   else
-    down<false>(bm, g, grid, stream);
+    down<false>(bm, once, g, grid, stream);
   return hipGetLastError();
 }
 

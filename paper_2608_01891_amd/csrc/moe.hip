@@ -268,7 +268,7 @@ hipError_t launch_moe_experts(const aflex_ffn_args& f, void* route_ws, void* exp
   g.mt_major = 0;  // an expert's m-tiles are adjacent: overflow tiles re-read its weights from L2
   g.C = h;
   g.ldc = f.I;
-  e = launch_gate_up(L.bm, g, stream);
+  e = launch_gate_up(L.bm, false, g, stream);
   if (e != hipSuccess) return e;
 
   const long long pairs = (long long)f.T * f.k;
@@ -290,7 +290,7 @@ hipError_t launch_moe_experts(const aflex_ffn_args& f, void* route_ws, void* exp
   d.P = P;
   d.p_split_stride = pairs * f.H;
   d.ldp = f.H;
-  e = launch_down(L.bm, true, d, stream);
+  e = launch_down(L.bm, true, false, d, stream);
   if (e != hipSuccess) return e;
 
   dim3 grid(f.T, (f.H / 4 + 255) / 256);
