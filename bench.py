@@ -378,7 +378,10 @@ def main():
         # token, attention, output projection [64, 8192] x [5120, 8192]^T.
         kn = synth.normal_tensor(1, 40, (wq.B, wq.Hkv, wq.D), device=dev)
         vn = synth.normal_tensor(1, 41, (wq.B, wq.Hkv, wq.D), device=dev)
-        w_o = synth.normal_tensor(1, 42, (5120, wq.Hq * wq.D), scale=0.02, device=dev)
+        # three copies of W_o (84 MB each) rotate with the KV pools, so the 256 MB
+        # last-level cache cannot serve the projection's weights from the previous call
+        w_os = [synth.normal_tensor(1, 42, (5120, wq.Hq * wq.D), scale=0.02, device=dev) for _ in range(3)]
+        w_o = w_os[0]
         y_o = torch.empty(wq.B, 5120, dtype=torch.bfloat16, device=dev)
         it[0] = 0
 
@@ -386,7 +389,7 @@ def main():
             c = copies[it[0] % 3]
             aflex.kv_append(c, kn, vn)
             aflex.attn_decode(c, out=outq)
-            aflex.linear(outq.view(wq.B, -1), w_o, y=y_o)
+            aflex.linear(outq.view(wq.B, -1), w_os[it[0] % 3], y=y_o)
             it[0] += 1
         for _ in range(3):
             run_stage()
@@ -397,7 +400,7 @@ def main():
             "hbm_frac": round(sbytes / (ms * 1e-3) / PEAK_HBM, 4), "bytes": sbytes,
             "tok_per_s": round(wq.B / (ms * 1e-3), 1),
             "kernels": kk}
-        del copies, wq, w_o
+        del copies, wq, w_o, w_os
 
         # Full-batch long-context attention of the pipeline workload
         outl = torch.empty(B, a.Hq, a.D, dtype=torch.bfloat16, device=dev)
