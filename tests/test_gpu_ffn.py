@@ -53,3 +53,12 @@ def test_qwen3_prefill_tokens_sampled(gpu_lib, qwen3_weights):
     rows = sample_rows(T, 6, seed=T, must=[0, 255, 256, T - 1])
     ref = oracle.swiglu_ffn(x[rows].cpu(), wg, wu, wd)
     check_rows(y[rows], ref, what="qwen3 swiglu prefill T=4096 (sampled)")
+
+
+@pytest.mark.parametrize("T", [32, 33, 64, 65, 255, 257])
+def test_tile_plan_boundaries(gpu_lib, T):
+    """Token counts on both sides of the dense tile-size thresholds and a
+    256-row tile with a one-row tail."""
+    x, w, _ = synth.custom_ffn(120 + T, T, 320, 640)
+    y = aflex.ffn_swiglu(x.to(DEV), w.to(DEV)).cpu()
+    check_rows(y, oracle.swiglu_ffn(x, w.w_gate, w.w_up, w.w_down), what=f"swiglu T={T}")

@@ -89,3 +89,25 @@ def test_mixtral_prefill_tokens_sampled(gpu_lib, mixtral):
     ref, _, _ = oracle.moe_ffn(wl.x.cpu(), wl.router_logits.cpu(), f.w_gate.cpu(), f.w_up.cpu(),
                                f.w_down.cpu(), 2, token_indices=toks)
     check_rows(y.cpu()[toks], ref[toks], what="mixtral moe prefill T=4096 (sampled)")
+
+
+@pytest.mark.parametrize("T,E,k", [(200, 64, 8), (33, 64, 1), (64, 2, 2)])
+def test_routing_extremes(gpu_lib, T, E, k):
+    """The largest supported expert count and top-k (E = 64, k = 8), top-1 over
+    64 experts (many empty experts), and k = E."""
+    H, I = 128, 128
+    x, w, logits = synth.custom_ffn(80 + E + k, T, H, I, E=E)
+    y, r = aflex.moe_ffn(x.to(DEV), w.to(DEV), logits.to(DEV), k, routing=True)
+    _check_routing(r, logits, k, E)
+    ref, _, _ = oracle.moe_ffn(x, logits, w.w_gate, w.w_up, w.w_down, k)
+    check_rows(y.cpu(), ref, what=f"moe extremes T={T} E={E} k={k}")
+
+
+@pytest.mark.parametrize("T", [20, 160, 600])
+def test_tile_shape_boundaries(gpu_lib, T):
+    """Row counts per expert on both sides of the tile-size thresholds (32-, 64-
+    and 256-row tiles) with 8 experts and top-2."""
+    x, w, logits = synth.custom_ffn(90 + T, T, 256, 192, E=8)
+    y = aflex.moe_ffn(x.to(DEV), w.to(DEV), logits.to(DEV), 2).cpu()
+    ref, _, _ = oracle.moe_ffn(x, logits, w.w_gate, w.w_up, w.w_down, 2)
+    check_rows(y, ref, what=f"moe tile boundary T={T}")

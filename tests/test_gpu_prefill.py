@@ -112,3 +112,27 @@ def test_prefill_then_decode_on_the_written_cache(gpu_lib):
     ref = oracle.attention_prefill(p.q.cpu(), p.k.cpu(), p.v.cpu(), p.cu_seqlens.cpu(), rows=last.tolist())
     check_rows(dec, ref[last], what="decode over the prefilled cache")
     check_rows(out[last], ref[last], what="prefill last rows")
+
+
+def test_long_prompt_sampled(gpu_lib):
+    """One 16384-token prompt at the Qwen3-32B head shape (longer than any of the
+    paper's inputs): sampled rows, including the last."""
+    n = 16384
+    p = synth.make_prefill(55, [n], 64, 8, 128, device=DEV)
+    out = aflex.attn_prefill(p).cpu()
+    pc = p.to("cpu")
+    rows = sample_rows(n, 4, seed=5, must=[0, 8191, n - 1])
+    ref = oracle.attention_prefill(pc.q, pc.k, pc.v, pc.cu_seqlens, rows=rows)
+    check_rows(out[rows], ref[rows], what="prefill n=16384 (sampled)")
+
+
+def test_kv_write_long_prompt_bit_exact(gpu_lib):
+    n = 5000
+    a = synth.custom_attention(56, 1, 8, 8, 128, [n], ctx_hi=n)
+    kn = synth.normal_tensor(56, 42, (n, 8, 128))
+    vn = synth.normal_tensor(56, 43, (n, 8, 128))
+    cu = torch.tensor([0, n], dtype=torch.int32)
+    rk, rv = oracle.kv_write(a.k_cache, a.v_cache, a.block_table, a.context_lens, cu, kn, vn)
+    ad = a.to(DEV)
+    aflex.kv_write(ad, kn.to(DEV), vn.to(DEV), cu.to(DEV), max_seqlen=n)
+    assert torch.equal(ad.k_cache.cpu(), rk) and torch.equal(ad.v_cache.cpu(), rv)
