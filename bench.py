@@ -350,6 +350,24 @@ def main():
             "measured_choice": "+".join(map(str, best)), "measured_ms": round(meas[best], 4),
             "measured_tok_per_s": round(B / (meas[best] * 1e-3), 1)}
         variants["t_F_over_t_A"] = round(t_f / t_a, 3)
+        # A and F pools on one GPU: the two stages' streams on disjoint CU sets
+        pools = {}
+        for acu in (64, 128, 192):
+            pa, pf = aflex.pool_streams(acu, dev)
+            for M in (2, 4):
+                m = plan.equal_microbatches(B, M)
+
+                def pstep():
+                    aflex.af_pipeline_step(a, f, logits, k, m, y=y, stream_a=pa, stream_f=pf, ws=pws, join=False)
+                pstep()
+                torch.cuda.synchronize()
+                t0 = time.perf_counter()
+                for _ in range(5):
+                    pstep()
+                torch.cuda.synchronize()
+                pms = (time.perf_counter() - t0) * 1e3 / 5
+                pools[f"attn_cus={acu},M={M}"] = {"ms": round(pms, 4), "tok_per_s": round(B / (pms * 1e-3), 1)}
+        variants["cu_pools"] = pools
         ops["af_pipeline"] = variants
 
         # Qwen3-32B decode attention, 3 KV-pool copies rotated so the 256 MB MALL cannot hold them

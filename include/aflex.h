@@ -257,6 +257,20 @@ typedef struct aflex_prefill_args {
 /* position max_seqlen are not written. Empty prompts produce no rows.        */
 aflex_status aflex_attn_prefill(const aflex_prefill_args *a, aflex_stream stream);
 
+/* Two streams whose kernels run on disjoint sets of compute units: the       */
+/* single-GPU analogue of the paper's separate Attention and FFN GPU pools    */
+/* (section 4.1, section 4.3) for aflex_af_pipeline_step. attn_cus of the 256 */
+/* CUs serve stream_a, the others stream_f; attn_cus must be 64, 128 or 192.  */
+/* Each XCD gives the same share of its CUs to each pool (the masks take bit  */
+/* i for the attention pool when (i / 8) % 4 < attn_cus / 64, which is even   */
+/* per XCD whether CU bits are numbered XCD by XCD or interleaved across     */
+/* XCDs). Streams have the default priority. The caller releases them with   */
+/* aflex_pool_streams_destroy. Errors: INVALID_ARG for NULL outputs,          */
+/* UNSUPPORTED for another attn_cus or a device without 256 CUs, HIP when     */
+/* stream creation fails (nothing is left allocated then).                    */
+aflex_status aflex_pool_streams_create(int32_t attn_cus, aflex_stream *stream_a, aflex_stream *stream_f);
+aflex_status aflex_pool_streams_destroy(aflex_stream stream_a, aflex_stream stream_f);
+
 /* ------------------------------------------------------------------------ */
 /* Per-kernel timing, the single-GPU analogue of the paper's per-operator     */
 /* latency profiling (section 4.1; section 5, "Profiling module"). Between    */

@@ -110,6 +110,8 @@ def load():
         "aflex_linear": [ctypes.POINTER(LinearArgs), _p, ctypes.c_size_t, _p],
         "aflex_attn_prefill": [ctypes.POINTER(PrefillArgs), _p],
         "aflex_kv_write": [ctypes.POINTER(KvWriteArgs), _p],
+        "aflex_pool_streams_create": [ctypes.c_int32, ctypes.POINTER(_p), ctypes.POINTER(_p)],
+        "aflex_pool_streams_destroy": [_p, _p],
     }
     for name, args in sig.items():
         fn = getattr(lib, name)
@@ -337,6 +339,24 @@ def pipeline_streams(device):
     if d not in _pipe_streams:
         _pipe_streams[d] = (torch.cuda.Stream(device=d), torch.cuda.Stream(device=d))
     return _pipe_streams[d]
+
+
+_pool_streams = {}
+
+
+def pool_streams(attn_cus: int, device="cuda:0"):
+    """Stream pair on disjoint CU sets (attn_cus of 256 CUs for the attention stage),
+    as torch external streams; created once per (device, attn_cus), kept for the process."""
+    d = torch.device(device)
+    key = (d, attn_cus)
+    if key not in _pool_streams:
+        lib = load()
+        with torch.cuda.device(d):
+            sa, sf = _p(), _p()
+            _check(lib.aflex_pool_streams_create(attn_cus, ctypes.byref(sa), ctypes.byref(sf)))
+        _pool_streams[key] = (torch.cuda.ExternalStream(sa.value, device=d),
+                              torch.cuda.ExternalStream(sf.value, device=d))
+    return _pool_streams[key]
 
 
 def af_pipeline_step(a, w, logits, k: int, mb_sizes, L: int = 1, y=None, stream_a=None,

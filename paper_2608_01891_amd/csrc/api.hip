@@ -190,6 +190,46 @@ aflex_status aflex_kv_append(const aflex_kv_append_args* a, aflex_stream stream)
   return hip_status(aflex::launch_kv_append(*a, (hipStream_t)stream), "kv_append");
 }
 
+aflex_status aflex_pool_streams_create(int32_t attn_cus, aflex_stream* stream_a, aflex_stream* stream_f) {
+  REQUIRE(stream_a && stream_f, AFLEX_ERR_INVALID_ARG, "pool streams: NULL output");
+  *stream_a = nullptr;
+  *stream_f = nullptr;
+  REQUIRE(attn_cus == 64 || attn_cus == 128 || attn_cus == 192, AFLEX_ERR_UNSUPPORTED,
+          "pool streams: attn_cus %d must be 64, 128 or 192", attn_cus);
+  int dev = 0, ncu = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e == hipSuccess) e = hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev);
+  if (e != hipSuccess) return hip_status(e, "pool streams");
+  REQUIRE(ncu == 256, AFLEX_ERR_UNSUPPORTED, "pool streams: device has %d CUs (256 expected)", ncu);
+  uint32_t ma[8] = {0}, mf[8] = {0};
+  for (int i = 0; i < 256; ++i) {
+    if ((i / 8) % 4 < attn_cus / 64)
+      ma[i / 32] |= 1u << (i % 32);
+    else
+      mf[i / 32] |= 1u << (i % 32);
+  }
+  hipStream_t sa = nullptr, sf = nullptr;
+  e = hipExtStreamCreateWithCUMask(&sa, 8, ma);
+  if (e == hipSuccess) e = hipExtStreamCreateWithCUMask(&sf, 8, mf);
+  if (e != hipSuccess) {
+    if (sa) (void)hipStreamDestroy(sa);
+    return hip_status(e, "pool streams");
+  }
+  *stream_a = sa;
+  *stream_f = sf;
+  return AFLEX_OK;
+}
+
+aflex_status aflex_pool_streams_destroy(aflex_stream stream_a, aflex_stream stream_f) {
+  hipError_t e = hipSuccess;
+  if (stream_a) e = hipStreamDestroy((hipStream_t)stream_a);
+  if (stream_f) {
+    const hipError_t e2 = hipStreamDestroy((hipStream_t)stream_f);
+    if (e == hipSuccess) e = e2;
+  }
+  return hip_status(e, "pool streams");
+}
+
 aflex_status aflex_kv_write(const aflex_kv_write_args* a, aflex_stream stream) {
   REQUIRE(a, AFLEX_ERR_INVALID_ARG, "kv_write: args is NULL");
   REQUIRE(a->k_new && a->v_new && a->cu_seqlens && a->k_cache && a->v_cache && a->block_table && a->context_lens,

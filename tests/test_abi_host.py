@@ -21,7 +21,7 @@ def lib():
 
 def test_exports_every_declared_symbol(lib):
     names = aflex.exported_names()
-    assert len(names) == 19
+    assert len(names) == 21
     for n in names:
         assert hasattr(lib, n), n
     assert lib.aflex_version().startswith(b"aflex")
@@ -177,3 +177,12 @@ def test_kv_write_validation(lib):
         a = mk(**kw)
         assert lib.aflex_kv_write(ctypes.byref(a), None) == st, kw
         assert lib.aflex_last_error().startswith(b"kv_write")
+
+
+def test_pool_streams_validation(lib):
+    sa = ctypes.c_void_p()
+    assert lib.aflex_pool_streams_create(128, None, ctypes.byref(sa)) == aflex.ERR_INVALID_ARG
+    assert lib.aflex_last_error().startswith(b"pool streams")
+    sf = ctypes.c_void_p()
+    assert lib.aflex_pool_streams_create(100, ctypes.byref(sa), ctypes.byref(sf)) == aflex.ERR_UNSUPPORTED
+    assert sa.value is None and sf.value is None

@@ -61,3 +61,20 @@ def test_af_pipeline_workload_sampled(gpu_lib):
     check_rows(y4[rows], ref, what="A/F pipeline M=4 (sampled)")
     check_rows(y1[rows], ref, what="A/F pipeline M=1 (sampled)")
     check_rows(y4, y1.double(), what="M=4 vs M=1 over all rows")
+
+
+@pytest.mark.parametrize("attn_cus", [64, 128, 192])
+def test_cu_pool_streams_same_result(gpu_lib, attn_cus):
+    """The step on CU-partitioned streams (attention pool and FFN pool) gives the
+    bitwise result of the step on ordinary streams: placement changes no
+    arithmetic."""
+    a, w, logits = _small()
+    ad, wd, ld = a.to(DEV), w.to(DEV), logits.to(DEV)
+    ref = aflex.af_pipeline_step(ad, wd, ld, 2, [3, 5], L=2).clone()
+    sa, sf = aflex.pool_streams(attn_cus, DEV)
+    cur = torch.cuda.current_stream()
+    sa.wait_stream(cur); sf.wait_stream(cur)
+    y = aflex.af_pipeline_step(ad, wd, ld, 2, [3, 5], L=2, stream_a=sa, stream_f=sf)
+    cur.wait_stream(sf)
+    torch.cuda.synchronize()
+    assert torch.equal(y, ref)
