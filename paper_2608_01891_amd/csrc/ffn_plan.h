@@ -6,17 +6,20 @@
 
 namespace aflex {
 
-// Output columns per gate/up tile (x2 weight rows) and per down tile.
-inline int gate_bn(int bm) { return bm >= 256 ? 128 : 64; }
+// Output columns per gate/up tile (x2 weight rows) and per down tile. The
+// 128- and 256-row tiles are the 8-wave 32x32x16 MFMA shapes (one work-group
+// per CU); dense GEMMs take 128-row tiles for 33 ... 128 tokens (measured:
+// T = 128 262 -> 211 us against 256-row tiles), MoE GEMMs never do.
+inline int gate_bn(int bm) { return bm >= 128 ? 128 : 64; }
 
-inline int down_bn(int bm) { return bm >= 256 ? 256 : 128; }
+inline int down_bn(int bm) { return bm >= 128 ? 256 : 128; }
 // Work-groups the down GEMM's split-K aims for: the 256-row tiles run one
 // work-group per CU, so one round of the chip; smaller tiles two per CU.
 constexpr int kOneWgPerCuTarget = 256;
-inline int down_target(int bm) { return bm >= 256 ? kOneWgPerCuTarget : (bm == 64 ? 2048 : 512); }
+inline int down_target(int bm) { return bm >= 128 ? kOneWgPerCuTarget : (bm == 64 ? 2048 : 512); }
 
 struct FfnPlan {
-  int bm;           // rows per m-tile: 32, 64 or 256
+  int bm;           // rows per m-tile: 32, 64, 128 or 256
   int down_splits;  // split-K factor of the down GEMM
   int down_kps;     // k elements per split (multiple of 64)
 };
@@ -67,7 +70,7 @@ inline void plan_splits(int base_tiles, int K, int target, int min_steps, int* s
 
 inline FfnPlan plan_dense(int T, int H, int I) {
   FfnPlan pl;
-  pl.bm = T <= 32 ? 32 : (T <= 64 ? 64 : 256);
+  pl.bm = T <= 32 ? 32 : (T <= 128 ? 128 : 256);
   const int mtiles = (T + pl.bm - 1) / pl.bm;
   const int ntiles = (H + down_bn(pl.bm) - 1) / down_bn(pl.bm);
   plan_splits(mtiles * ntiles, I, down_target(pl.bm), 8, &pl.down_splits, &pl.down_kps);

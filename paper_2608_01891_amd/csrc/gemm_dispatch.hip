@@ -1,13 +1,14 @@
 // Instantiations of the FFN GEMM tiles and their launch helpers.
 //
 // Row-tile size selects the shape: 32- and 64-row tiles stream weights (4
-// waves, 16x16x32 MFMA, 64-wide k-steps, two work-groups per CU, HBM-bound;
-// weights that one tile streams exactly once load non-temporally: always for
-// 32-row tiles, for 64-row tiles when the caller has a single row tile);
-// 256-row tiles are the MFMA-bound shape (8 waves with 128 x 64 wave tiles
-// (gate/up: 128 x 32 of each weight matrix) of 32x32x16 MFMAs, 32-wide
-// k-steps, a ring of five stages in the whole 160 KiB of LDS, one work-group
-// per CU).
+// waves, 16x16x32 MFMA, 64-wide k-steps, two work-groups per CU, HBM-bound);
+// 128- and 256-row tiles are the 8-wave 32x32x16 MFMA shapes (wave tiles of
+// 64 or 128 rows by 32 columns of each gate/up matrix or 64 columns of the
+// down matrix, 32-wide k-steps, a ring of five or six stages in the whole 160
+// KiB of LDS, one work-group per CU). Weights that one tile streams exactly
+// once load non-temporally: always for 32-row tiles, for 64-row tiles when
+// the caller has a single row tile (on the 8-wave tiles it was measured
+// slower: dense T = 128 211 -> 285 us).
 #include "ffn_plan.h"
 #include "profile.h"
 
@@ -34,6 +35,7 @@ hipError_t launch_gate_up(int bm, bool once, const GemmParams& g, hipStream_t st
       else
         go<64, 64, 2, 2, 64, 16, true, false, 81920>(g, grid, stream);
       break;
+    case 128: go<128, 128, 2, 4, 32, 32, true, false, 163840>(g, grid, stream); break;
     default: go<256, 128, 2, 4, 32, 32, true, false, 163840>(g, grid, stream); break;
   }
   return hipGetLastError();
@@ -49,6 +51,7 @@ static void down(int bm, bool once, const GemmParams& g, unsigned grid, hipStrea
       else
         go<64, 128, 2, 2, 64, 16, false, F32, 81920>(g, grid, stream);
       break;
+    case 128: go<128, 256, 2, 4, 32, 32, false, F32, 163840>(g, grid, stream); break;
     default: go<256, 256, 2, 4, 32, 32, false, F32, 163840>(g, grid, stream); break;
   }
 }
