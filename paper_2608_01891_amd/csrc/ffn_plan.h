@@ -9,7 +9,7 @@ namespace aflex {
 // Output columns per gate/up tile (x2 weight rows) and per down tile. The
 // 128- and 256-row tiles are the 8-wave 32x32x16 MFMA shapes (one work-group
 // per CU); dense GEMMs take 128-row tiles for 33 ... 128 tokens (measured:
-// T = 128 262 -> 211 us against 256-row tiles), MoE GEMMs never do.
+// T = 128 262 -> 211 us against 256-row tiles).
 inline int gate_bn(int bm) { return bm >= 128 ? 128 : 64; }
 
 inline int down_bn(int bm) { return bm >= 128 ? 256 : 128; }
@@ -26,12 +26,14 @@ struct FfnPlan {
 
 // Rows per m-tile for grouped GEMMs with the given average rows per expert.
 // Up to 32 rows a tile covers a typical expert (its weights are streamed once,
-// non-temporally); up to 160 rows 64-row tiles, two work-groups per CU (an
-// expert's second and third tiles re-read its weights from L2; measured
-// faster than one 128-row tile per CU); beyond, the MFMA-bound 256-row shape.
+// non-temporally); up to 72 rows 64-row tiles, two work-groups per CU (an
+// expert's second tile re-reads its weights from L2); up to 160 rows the
+// 8-wave 128-row tile (measured T = 512: 890 -> 830 us against 64-row
+// tiles); beyond, the 256-row shape.
 inline int pick_bm(double rows_per_expert) {
   if (rows_per_expert * 1.3 <= 32) return 32;
-  if (rows_per_expert <= 160) return 64;
+  if (rows_per_expert <= 72) return 64;
+  if (rows_per_expert <= 160) return 128;
   return 256;
 }
 
