@@ -176,10 +176,18 @@ class Workspace:
 _default_ws = {}
 
 
-def _ws(key, nbytes, device, ws):
+def _ws(key, nbytes, device, ws, streams=()):
+    """Workspace pointer and size. The buffer comes from torch's caching allocator
+    on the current stream; its use on any other stream is recorded, so that a
+    later growth (which frees it) cannot hand the memory out while that stream
+    still reads it."""
     if ws is None:
         ws = _default_ws.setdefault(key, Workspace())
     buf = ws.get(nbytes, device)
+    cur = torch.cuda.current_stream(buf.device)
+    for s in streams:
+        if s is not None and s != cur:
+            buf.record_stream(s)
     return ctypes.c_void_p(buf.data_ptr()), ctypes.c_size_t(buf.numel())
 
 
@@ -211,7 +219,7 @@ def attn_decode(a, out=None, split_tokens: int = 0, scale: float = 0.0, stream=N
     args = attn_args(a, out, split_tokens, scale)
     n = ctypes.c_size_t()
     _check(lib.aflex_attn_decode_workspace(ctypes.byref(args), ctypes.byref(n)))
-    p, sz = _ws("attn", n.value, a.q.device, ws)
+    p, sz = _ws("attn", n.value, a.q.device, ws, (stream,))
     _check(lib.aflex_attn_decode(ctypes.byref(args), p, sz, _stream(stream)))
     return out
 
@@ -223,7 +231,7 @@ def ffn_swiglu(x, w, y=None, stream=None, ws=None):
     args = ffn_args(x, w, y)
     n = ctypes.c_size_t()
     _check(lib.aflex_ffn_swiglu_workspace(ctypes.byref(args), ctypes.byref(n)))
-    p, sz = _ws("ffn", n.value, x.device, ws)
+    p, sz = _ws("ffn", n.value, x.device, ws, (stream,))
     _check(lib.aflex_ffn_swiglu(ctypes.byref(args), p, sz, _stream(stream)))
     return y
 
@@ -243,7 +251,7 @@ def moe_ffn(x, w, logits, k: int, y=None, routing: bool = False, stream=None, ws
     args = ffn_args(x, w, y, logits, k, r)
     n = ctypes.c_size_t()
     _check(lib.aflex_moe_ffn_workspace(ctypes.byref(args), ctypes.byref(n)))
-    p, sz = _ws("moe", n.value, x.device, ws)
+    p, sz = _ws("moe", n.value, x.device, ws, (stream,))
     _check(lib.aflex_moe_ffn(ctypes.byref(args), p, sz, _stream(stream)))
     return (y, r) if routing else y
 
@@ -298,7 +306,7 @@ def linear(x, w, y=None, stream=None, ws=None):
     args = LinearArgs(x=_ptr(x), w=_ptr(w), y=_ptr(y), T=T, K=K, N=N)
     n = ctypes.c_size_t()
     _check(lib.aflex_linear_workspace(ctypes.byref(args), ctypes.byref(n)))
-    p, sz = _ws("linear", n.value, x.device, ws)
+    p, sz = _ws("linear", n.value, x.device, ws, (stream,))
     _check(lib.aflex_linear(ctypes.byref(args), p, sz, _stream(stream)))
     return y
 
@@ -325,7 +333,7 @@ def moe_block(x, w, norm_weight, router_weight, k: int, eps: float = 1e-5, resid
                         router_logits_out=_ptr(logits))
     n = ctypes.c_size_t()
     _check(lib.aflex_moe_block_workspace(ctypes.byref(args), ctypes.byref(n)))
-    p, sz = _ws("moe_block", n.value, x.device, ws)
+    p, sz = _ws("moe_block", n.value, x.device, ws, (stream,))
     _check(lib.aflex_moe_block(ctypes.byref(args), p, sz, _stream(stream)))
     return (y, logits, r) if routing else y
 
@@ -382,7 +390,7 @@ def af_pipeline_step(a, w, logits, k: int, mb_sizes, L: int = 1, y=None, stream_
     n = ctypes.c_size_t()
     _check(lib.aflex_af_pipeline_workspace(ctypes.byref(aa), ctypes.byref(fa), M, mb, L,
                                            ctypes.byref(n)))
-    p, sz = _ws("pipe", n.value, a.q.device, ws)
+    p, sz = _ws("pipe", n.value, a.q.device, ws, (stream_a, stream_f))
     _check(lib.aflex_af_pipeline_step(ctypes.byref(aa), ctypes.byref(fa), M, mb, L, p, sz,
                                       _stream(stream_a), _stream(stream_f)))
     if join:
