@@ -50,6 +50,8 @@ def parse():
     p.add_argument("--no-operators", action="store_true", help="skip the per-operator section")
     p.add_argument("--counters-pass", action="store_true",
                    help="only warm-up + steps of the layer step and a 1 GiB copy (for rocprofv3 --pmc)")
+    p.add_argument("--ffn-counters-pass", action="store_true",
+                   help="only the MFMA-bound FFN shapes (Qwen3 SwiGLU T=512, Mixtral MoE T=2048), for rocprofv3 --pmc")
     return p.parse_args()
 
 
@@ -145,6 +147,23 @@ def main():
     def step(m=mbs):
         aflex.af_pipeline_step(a, f, logits, k, m, y=y, stream_a=sa, stream_f=sf, ws=pws, join=False)
 
+    if args.ffn_counters_pass:
+        # Counter collection for the MFMA-bound FFN GEMMs: a few calls of each shape.
+        wd = synth.make_ffn_weights(2, 5120, 25600, device=dev)
+        w512 = synth.qwen3_swiglu(512, device=dev, weights=wd)
+        for _ in range(3):
+            aflex.ffn_swiglu(w512.x, wd)
+        torch.cuda.synchronize()
+        print("ffn counters pass: dense SwiGLU T=512 done", flush=True)
+        del wd
+        w2k = synth.mixtral_moe(device=dev, T=2048, seed=103, weights=f)
+        for _ in range(3):
+            aflex.moe_ffn(w2k.x, w2k.ffn, w2k.router_logits, 2)
+        torch.cuda.synchronize()
+        print("ffn counters pass: MoE T=2048 done", flush=True)
+        print(json.dumps({"ffn_counters_pass": True}))
+        return
+
     if args.counters_pass:
         # Counter collection serialises dispatches; it runs the FFN stage's kernels
         # at the pipeline's microbatch shape on one stream (no cross-stream waits),
@@ -183,7 +202,9 @@ def main():
     ms_step = (t1 - t0) * 1e3 / args.steps
 
     # same steps again with HIP events around the dominant kernel on its stream
-    aflex.profile_start([DOMINANT, "attn_split", "gemm_down"])
+    STAGE_A = ("attn_split", "attn_merge")
+    STAGE_F = ("moe_route", DOMINANT, "gemm_down", "moe_combine")
+    aflex.profile_start(list(STAGE_A + STAGE_F))
     t2 = time.perf_counter()
     for _ in range(args.steps):
         step()
@@ -249,6 +270,25 @@ def main():
     }
     result["kernels_in_step"] = {kname: {"launches": v[0], "avg_ms": round(v[1] / v[0], 5)}
                                  for kname, v in prof.items()}
+    # Busy fraction of each stage's stream over the step (kernel time per step /
+    # step time measured with the same events): the single-GPU analogue of the
+    # paper's A/F idle time (section 3.3), with both stages sharing one GPU.
+    steps_ev = args.steps
+    busy = {}
+    for stage, names in (("attention_stream", STAGE_A), ("ffn_stream", STAGE_F)):
+        ms_k = sum(prof[n][1] for n in names if n in prof) / steps_ev
+        busy[stage] = {"kernel_ms_per_step": round(ms_k, 4), "busy_fraction": round(ms_k / ms_step_ev, 4)}
+    result["stage_busy"] = busy
+
+    # Plain device-to-device copy of 4 GiB (2 GiB read + 2 GiB written): the
+    # achievable-HBM reference of this run, next to the 8 TB/s nameplate.
+    src = torch.empty(1 << 30, dtype=torch.int16, device=dev)
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    ms_copy = timed(lambda: dst.copy_(src), 5)
+    result["hbm_reference"] = {"copy_GB_per_s": round(4 * (1 << 30) / (ms_copy * 1e-3) / 1e9, 1),
+                               "note": "read + write bytes of a 2 GiB device copy / time"}
+    del src, dst
 
     # ---------------- energy per token (where the counter is readable) -------------
     read_energy = energy_reader()
