@@ -410,6 +410,18 @@ def main():
         variants["cu_pools"] = pools
         ops["af_pipeline"] = variants
 
+        # Tiny decoder layer (B=4, 8/2 heads x 64, SwiGLU 512 -> 1408): cache-resident,
+        # so its lines are latencies
+        wt = synth.tiny_layer(device=dev)
+        ot = aflex.attn_decode(wt.attn)
+        yt = aflex.ffn_swiglu(wt.x, wt.ffn)
+        ms_a, kk_a = timed_kernels(lambda: aflex.attn_decode(wt.attn, out=ot), 50, ["attn_split", "attn_merge"], aflex)
+        ms_f, kk_f = timed_kernels(lambda: aflex.ffn_swiglu(wt.x, wt.ffn, y=yt), 50,
+                                   ["gemm_gate_up", "gemm_down", "splitk_reduce"], aflex)
+        ops["tiny_layer"] = {"attention_ms": round(ms_a, 5), "swiglu_ms": round(ms_f, 5),
+                             "attention_kernels": kk_a, "swiglu_kernels": kk_f}
+        del wt, ot, yt
+
         # Qwen3-32B decode attention, 3 KV-pool copies rotated so the 256 MB MALL cannot hold them
         wq = synth.qwen3_attention(device=dev).attn
         copies = [wq] + [synth.AttnInputs(**{**wq.__dict__, "k_cache": wq.k_cache.clone(),
