@@ -582,6 +582,40 @@ def main():
             "mfma_frac": round(flops / (ms * 1e-3) / PEAK_BF16, 4), "tok_per_s": round(Tp / (ms * 1e-3), 1),
             "kernels": kk}
         del wm, yp
+        # Resource sensitivity per operator: the same call on 64, 128, 192 and all
+        # 256 CUs (CU-masked streams). The single-GPU analogue of the paper's
+        # per-operator frequency sensitivity (section 3.2: decode attention gains
+        # little from more GPU clock, the FFN a lot); reduction = 1 - t(256) / t(64).
+        sens = {}
+        wd = synth.make_ffn_weights(2, 5120, 25600, device=dev)
+        wq = synth.qwen3_attention(device=dev).attn
+        oq = torch.empty(wq.B, wq.Hq, wq.D, dtype=torch.bfloat16, device=dev)
+        x32 = synth.qwen3_swiglu(32, device=dev, weights=wd).x
+        x512 = synth.qwen3_swiglu(512, device=dev, weights=wd).x
+        y32 = torch.empty(32, 5120, dtype=torch.bfloat16, device=dev)
+        y512 = torch.empty(512, 5120, dtype=torch.bfloat16, device=dev)
+        pw = synth.prefill_workload("qwen3-32b", 4096, 2, device=dev)
+        op_ = torch.empty_like(pw.q)
+        cases = {
+            "decode_attention_qwen3_B64": lambda st: aflex.attn_decode(wq, out=oq, stream=st, ws=wss["a"]),
+            "decode_swiglu_qwen3_T32": lambda st: aflex.ffn_swiglu(x32, wd, y=y32, stream=st, ws=wss["f"]),
+            "decode_swiglu_qwen3_T512": lambda st: aflex.ffn_swiglu(x512, wd, y=y512, stream=st, ws=wss["f"]),
+            "prefill_attention_qwen3_2x4096": lambda st: aflex.attn_prefill(pw, out=op_, stream=st),
+        }
+        wss = {"a": aflex.Workspace(), "f": aflex.Workspace()}
+        for name, fn in cases.items():
+            row = {}
+            for cus in (64, 128, 192, 256):
+                st = aflex.pool_streams(cus, dev)[0] if cus < 256 else torch.cuda.current_stream()
+                st.wait_stream(torch.cuda.current_stream())
+                fn(st)
+                row[f"{cus}_cus_ms"] = round(timed(lambda: fn(st), 10, stream=st), 5)
+                torch.cuda.current_stream().wait_stream(st)
+            row["reduction_64_to_256"] = round(1 - row["256_cus_ms"] / row["64_cus_ms"], 3)
+            sens[name] = row
+        torch.cuda.synchronize()
+        ops["cu_sensitivity"] = sens
+        del wd, wq, oq, x32, x512, y32, y512, pw, op_
         result["operators"] = ops
 
     # ---------------- CPU baseline: the oracle on a bounded sample -------------------
