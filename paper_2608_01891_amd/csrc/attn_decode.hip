@@ -291,10 +291,15 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnParams p) {
 
 int attn_split_tokens(const aflex_attn_args& a) {
   if (a.split_tokens > 0) return a.split_tokens;
-  // Enough work-groups to keep every CU busy several times over, otherwise
-  // fewer, longer splits (less partial-result traffic).
-  const long per512 = (long)a.B * a.Hkv * ((a.max_context_len + 511) / 512);
-  return per512 >= 4096 ? 512 : 256;
+  // Longer splits amortise each work-group's fixed cost (the block-id and q
+  // loads ahead of its first K/V byte, the LDS merge, the partial write and
+  // the merge kernel's share) but leave fewer work-groups to fill 256 CUs.
+  // The context lengths stay on the device, so the work-group count is
+  // bounded through max_context_len: the longest split whose bound still
+  // leaves several rounds of work-groups.
+  const long kv_rows = (long)a.B * a.Hkv;
+  if (kv_rows * ((a.max_context_len + 1023) / 1024) >= 8192) return 1024;
+  return kv_rows * ((a.max_context_len + 511) / 512) >= 4096 ? 512 : 256;
 }
 
 static int max_splits_of(const aflex_attn_args& a, int S) {

@@ -32,6 +32,16 @@ def test_ragged_multi_split(gpu_lib, D, Hq, Hkv, split):
     check_rows(out, _oracle(a), what=f"ragged D={D} G={Hq // Hkv} split={split}")
 
 
+@pytest.mark.parametrize("split", [1024, 0])
+def test_full_1024_token_splits(gpu_lib, split):
+    """Splits of 64 blocks (every lane of a wave holds a block id), exact and
+    ragged multiples of the split, with 8 query heads per KV head."""
+    ctx = [1024, 1025, 2047, 2048, 3000, 5, 64, 4100]
+    a = synth.custom_attention(32, len(ctx), 64, 8, 128, ctx, ctx_hi=4200)
+    out = aflex.attn_decode(a.to(DEV), split_tokens=split).cpu()
+    check_rows(out, _oracle(a), what=f"1024-token splits (split={split})")
+
+
 def test_qwen3_shape_sampled(gpu_lib):
     w = synth.qwen3_attention(device=DEV)
     a = w.attn
