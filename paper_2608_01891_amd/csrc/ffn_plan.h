@@ -17,6 +17,9 @@ inline int down_bn(int bm) { return bm >= 128 ? 256 : 128; }
 // work-group per CU, so one round of the chip; smaller tiles two per CU.
 constexpr int kOneWgPerCuTarget = 256;
 inline int down_target(int bm) { return bm >= 128 ? kOneWgPerCuTarget : (bm == 64 ? 2048 : 512); }
+// Work-groups resident on the 256 CUs at once: one per CU for the 8-wave
+// tiles (the whole LDS), two for the 4-wave tiles.
+inline int concurrent_wgs(int bm) { return bm >= 128 ? 256 : 512; }
 
 struct FfnPlan {
   int bm;           // rows per m-tile: 32, 64, 128 or 256
@@ -38,22 +41,24 @@ inline int pick_bm(double rows_per_expert) {
   return 256;
 }
 
-// Split K so that the down GEMM has about `target` work-groups, keeping at
-// least `min_steps` 64-wide k-steps per split. The 256-row tiles run one
-// work-group per CU, so for them the split count is the smallest that fills
-// the rounds of 256 CUs it needs to at least 90% (measured best for the dense
-// down GEMM at T = 256 ... 4096: 12, 6, 3, 3-4 splits); more splits only add
-// fp32 partials to reduce.
-inline void plan_splits(int base_tiles, int K, int target, int min_steps, int* splits, int* kps) {
+// Split K of the down GEMM, keeping at least `min_steps` 64-wide k-steps per
+// split. With `slots` > 0 (the tile count is exact: dense GEMMs, and the
+// one-work-group-per-CU tiles) the split count is the smallest whose
+// work-groups fill the rounds of `slots` concurrent work-groups they need to
+// at least 90% (measured best for the dense down GEMM at T = 256 ... 4096:
+// 12, 6, 3, 3-4 splits; a nearly empty last round leaves a few work-groups
+// streaming alone at the end); more splits only add fp32 partials to reduce.
+// Otherwise (a worst-case tile count) about `target` work-groups.
+inline void plan_splits(int base_tiles, int K, int target, int slots, int min_steps, int* splits, int* kps) {
   const int ksteps = K / 64;
   int smax = ksteps / min_steps;
   if (smax < 1) smax = 1;
   int s = (target + base_tiles - 1) / base_tiles;
-  if (target == kOneWgPerCuTarget) {
+  if (slots > 0) {
     double best_u = 0.0;
     for (int c = 1; c <= smax && c <= 64; ++c) {
       const long long wgs = (long long)base_tiles * c;
-      const double u = (double)wgs / (double)(((wgs + 255) / 256) * 256);
+      const double u = (double)wgs / (double)(((wgs + slots - 1) / slots) * slots);
       if (u >= 0.9) {
         s = c;
         break;
@@ -76,7 +81,7 @@ inline FfnPlan plan_dense(int T, int H, int I) {
   pl.bm = T <= 32 ? 32 : (T <= 128 ? 128 : 256);
   const int mtiles = (T + pl.bm - 1) / pl.bm;
   const int ntiles = (H + down_bn(pl.bm) - 1) / down_bn(pl.bm);
-  plan_splits(mtiles * ntiles, I, down_target(pl.bm), 8, &pl.down_splits, &pl.down_kps);
+  plan_splits(mtiles * ntiles, I, down_target(pl.bm), concurrent_wgs(pl.bm), 8, &pl.down_splits, &pl.down_kps);
   return pl;
 }
 

@@ -40,7 +40,10 @@ static MoeLayout moe_layout(const aflex_ffn_args& f) {
   L.bm = pick_bm((double)pairs / f.E);
   L.max_tiles = (int)((pairs + L.bm - 1) / L.bm) + f.E;
   const int ntiles = (f.H + down_bn(L.bm) - 1) / down_bn(L.bm);
-  plan_splits(L.max_tiles * ntiles, f.I, down_target(L.bm), 16, &L.down_splits, &L.down_kps);
+  // The tile count is a worst case here (the routing stays on the device):
+  // round filling only for the one-work-group-per-CU tiles, as measured.
+  plan_splits(L.max_tiles * ntiles, f.I, down_target(L.bm), L.bm >= 128 ? concurrent_wgs(L.bm) : 0, 16,
+              &L.down_splits, &L.down_kps);
   size_t o = 0;
   auto take = [&](size_t bytes) {
     size_t at = o;
