@@ -263,27 +263,46 @@ __global__ __launch_bounds__(64 * WM * WN, LDS_BYTES > 81920 ? 1 : 2) void gemm_
     AFLEX_GEMM_ISSUE(sm[((KT1) + STAGES - 1) % STAGES], (KT1) + STAGES - 1);              \
   } while (0)
 
-  // Software pipeline over k-chunks: the fragments of chunk c+1 are read while
-  // the MFMAs of chunk c run; a stage boundary's wait and barrier sit between
-  // the two, behind the in-flight MFMAs.
+  // Software pipeline over k-chunks (two per stage, so their count is even):
+  // the fragment reads of chunk c+1 are interleaved one by one with the MFMAs
+  // of chunk c (the wave issues in order, so a read placed between two MFMAs
+  // goes out while the first executes); the stage wait and barrier follow,
+  // then the reads of chunk c+2 interleaved with the MFMAs of chunk c+1. The
+  // body has no data-dependent guards, so the only LDS waits are for reads
+  // issued a chunk earlier; the last iteration's stage step and read of
+  // chunk c+2 re-read the last k-step (clamped), which is never used.
+  // Measured against the guarded two-chunk loop (whose waits covered the
+  // reads just issued): 4-5% at the MFMA-bound shapes, bit-identical.
   if (nk > 0) {
     bf16x8 fa0[TM], fb0[NB][TN], fa1[TM], fb1[NB][TN];
 #pragma unroll
     for (int st = 0; st < STAGES - 1; ++st) AFLEX_GEMM_ISSUE(sm[st], st);
     AFLEX_GEMM_STAGE(0);
     AFLEX_GEMM_READ(fa0, fb0, 0);
+    static_assert(CPS == 2, "two MFMA k-chunks per stage: the chunk count is even");
+    constexpr int NREAD = TM + NB * TN, NMMA = NB * TM * TN;
+    static_assert(NMMA >= NREAD, "interleave pattern");
     for (int c = 0; c < nchunks; c += 2) {
-      if (c + 1 < nchunks) {
-        if ((c + 1) % CPS == 0) AFLEX_GEMM_STAGE((c + 1) / CPS);
-        AFLEX_GEMM_READ(fa1, fb1, c + 1);
-      }
+      AFLEX_GEMM_READ(fa1, fb1, c + 1);
       AFLEX_GEMM_MMA(fa0, fb0);
-      if (c + 1 >= nchunks) break;
-      if (c + 2 < nchunks) {
-        if ((c + 2) % CPS == 0) AFLEX_GEMM_STAGE((c + 2) / CPS);
-        AFLEX_GEMM_READ(fa0, fb0, c + 2);
+#pragma unroll
+      for (int i = 0; i < NREAD; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
       }
+      __builtin_amdgcn_sched_group_barrier(0x008, NMMA - NREAD, 0);
+      __builtin_amdgcn_sched_barrier(0);
+      AFLEX_GEMM_STAGE((c + 2) / CPS);
+      __builtin_amdgcn_sched_barrier(0);
+      AFLEX_GEMM_READ(fa0, fb0, min(c + 2, nchunks - 1));
       AFLEX_GEMM_MMA(fa1, fb1);
+#pragma unroll
+      for (int i = 0; i < NREAD; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      }
+      __builtin_amdgcn_sched_group_barrier(0x008, NMMA - NREAD, 0);
+      __builtin_amdgcn_sched_barrier(0);
     }
     // no load may still target LDS when the work-group retires
     __builtin_amdgcn_s_waitcnt(0);
