@@ -13,8 +13,14 @@
  *   aflex_attn_decode       batched GQA decode attention over a paged KV cache
  *   aflex_ffn_swiglu        dense SwiGLU FFN (Qwen3-32B-shaped layers)
  *   aflex_moe_ffn           top-k mixture-of-experts SwiGLU FFN (Mixtral-8x7B)
+ *   aflex_moe_block         RMSNorm + router + MoE FFN (+ residual)
  *   aflex_af_pipeline_step  M microbatches of A then F on two HIP streams
+ *   aflex_kv_append         the new token's K/V into the paged cache
+ *   aflex_kv_write          a packed prompt's (or chunk's) K/V into the cache
+ *   aflex_linear            y = x W^T (the attention output projection)
  *   aflex_attn_prefill      causal attention over packed prompts (prefill)
+ *   aflex_pool_streams_*    stream pairs on disjoint CU sets (A/F pools)
+ *   aflex_profile_*         per-kernel HIP-event timing
  *
  * Conventions shared by every entry point
  *  - bf16 tensors are passed as raw bit patterns (aflex_bf16 = uint16_t).
@@ -113,7 +119,7 @@ typedef struct aflex_ffn_args {
   int32_t E, k;                 /* MoE only: experts and experts per token (ignored by dense) */
 } aflex_ffn_args;
 
-/* Supported: H and I multiples of 64, T >= 1; MoE 1 <= k <= E <= 64. */
+/* Supported: H and I multiples of 64, T >= 1; MoE 1 <= k <= E <= 64, k <= 8. */
 aflex_status aflex_ffn_swiglu_workspace(const aflex_ffn_args *f, size_t *bytes);
 aflex_status aflex_ffn_swiglu(const aflex_ffn_args *f, void *workspace, size_t workspace_bytes,
                               aflex_stream stream);
