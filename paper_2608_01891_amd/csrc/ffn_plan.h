@@ -85,8 +85,9 @@ inline FfnPlan plan_dense(int T, int H, int I) {
   return pl;
 }
 
-// `once`: the call has a single row tile per weight matrix, so every weight
-// byte is read exactly once (its loads can be non-temporal).
+// `once`: the call has (dense) or is expected to have (MoE, from the average
+// rows per expert) a single row tile per weight matrix, so every weight byte
+// is read once and its loads can be non-temporal.
 hipError_t launch_gate_up(int bm, bool once, const GemmParams& g, hipStream_t stream);
 hipError_t launch_down(int bm, bool f32_partials, bool once, const GemmParams& g, hipStream_t stream);
 

@@ -263,7 +263,7 @@ __global__ __launch_bounds__(64 * WM * WN, LDS_BYTES > 81920 ? 1 : 2) void gemm_
     AFLEX_GEMM_ISSUE(sm[((KT1) + STAGES - 1) % STAGES], (KT1) + STAGES - 1);              \
   } while (0)
 
-  // Software pipeline over k-chunks (two per stage, so their count is even):
+  // Software pipeline over k-chunks (an even number per stage):
   // the fragment reads of chunk c+1 are interleaved one by one with the MFMAs
   // of chunk c (the wave issues in order, so a read placed between two MFMAs
   // goes out while the first executes); the stage wait and barrier follow,
@@ -279,31 +279,35 @@ __global__ __launch_bounds__(64 * WM * WN, LDS_BYTES > 81920 ? 1 : 2) void gemm_
     for (int st = 0; st < STAGES - 1; ++st) AFLEX_GEMM_ISSUE(sm[st], st);
     AFLEX_GEMM_STAGE(0);
     AFLEX_GEMM_READ(fa0, fb0, 0);
-    static_assert(CPS == 2, "two MFMA k-chunks per stage: the chunk count is even");
+    static_assert(CPS % 2 == 0, "an even number of MFMA k-chunks per stage");
     constexpr int NREAD = TM + NB * TN, NMMA = NB * TM * TN;
     static_assert(NMMA >= NREAD, "interleave pattern");
-    for (int c = 0; c < nchunks; c += 2) {
-      AFLEX_GEMM_READ(fa1, fb1, c + 1);
-      AFLEX_GEMM_MMA(fa0, fb0);
+#define AFLEX_GEMM_INTERLEAVE()                                              \
+  do {                                                                       \
+    _Pragma("unroll") for (int i_ = 0; i_ < NREAD; ++i_) {                   \
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0); /* one MFMA */     \
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0); /* one LDS read */ \
+    }                                                                        \
+    __builtin_amdgcn_sched_group_barrier(0x008, NMMA - NREAD, 0);            \
+    __builtin_amdgcn_sched_barrier(0);                                       \
+  } while (0)
+    for (int kt = 0; kt < nk; ++kt) {
 #pragma unroll
-      for (int i = 0; i < NREAD; ++i) {
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      for (int cc = 0; cc < CPS; cc += 2) {
+        const int c = kt * CPS + cc;
+        AFLEX_GEMM_READ(fa1, fb1, c + 1);
+        AFLEX_GEMM_MMA(fa0, fb0);
+        AFLEX_GEMM_INTERLEAVE();
+        if (cc + 2 == CPS) {
+          AFLEX_GEMM_STAGE(kt + 1);
+          __builtin_amdgcn_sched_barrier(0);
+        }
+        AFLEX_GEMM_READ(fa0, fb0, min(c + 2, nchunks - 1));
+        AFLEX_GEMM_MMA(fa1, fb1);
+        AFLEX_GEMM_INTERLEAVE();
       }
-      __builtin_amdgcn_sched_group_barrier(0x008, NMMA - NREAD, 0);
-      __builtin_amdgcn_sched_barrier(0);
-      AFLEX_GEMM_STAGE((c + 2) / CPS);
-      __builtin_amdgcn_sched_barrier(0);
-      AFLEX_GEMM_READ(fa0, fb0, min(c + 2, nchunks - 1));
-      AFLEX_GEMM_MMA(fa1, fb1);
-#pragma unroll
-      for (int i = 0; i < NREAD; ++i) {
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-      }
-      __builtin_amdgcn_sched_group_barrier(0x008, NMMA - NREAD, 0);
-      __builtin_amdgcn_sched_barrier(0);
     }
+#undef AFLEX_GEMM_INTERLEAVE
     // no load may still target LDS when the work-group retires
     __builtin_amdgcn_s_waitcnt(0);
   }

@@ -4,11 +4,16 @@
 // waves, 16x16x32 MFMA, 64-wide k-steps, two work-groups per CU, HBM-bound);
 // 128- and 256-row tiles are the 8-wave 32x32x16 MFMA shapes (wave tiles of
 // 64 or 128 rows by 32 columns of each gate/up matrix or 64 columns of the
-// down matrix, 32-wide k-steps, a ring of five or six stages in the whole 160
-// KiB of LDS, one work-group per CU). Weights that one tile streams exactly
-// once load non-temporally: always for 32-row tiles, for 64-row tiles when
-// the caller has a single row tile (on the 8-wave tiles it was measured
-// slower: dense T = 128 211 -> 285 us).
+// down matrix, one work-group per CU in the whole 160 KiB of LDS). The
+// 128-row tiles take 64-wide k-steps (a ring of three stages), so every
+// k-step reads whole 128-byte lines of each weight row; the 256-row tiles
+// need 32-wide k-steps for a five-stage ring. Weights that one tile streams
+// exactly once load non-temporally: always for 32-row tiles, for 64- and
+// 128-row tiles when the caller has a single row tile per weight matrix
+// (measured on the 128-row tiles, dense T = 128: 215 -> 188 us for the
+// 64-wide k-steps, 175 us with non-temporal loads; with 32-wide k-steps
+// non-temporal loads were slower, the second half of each line then coming
+// from HBM again).
 #include "ffn_plan.h"
 #include "profile.h"
 
@@ -35,7 +40,12 @@ hipError_t launch_gate_up(int bm, bool once, const GemmParams& g, hipStream_t st
       else
         go<64, 64, 2, 2, 64, 16, true, false, 81920>(g, grid, stream);
       break;
-    case 128: go<128, 128, 2, 4, 32, 32, true, false, 163840>(g, grid, stream); break;
+    case 128:
+      if (once)
+        go<128, 128, 2, 4, 64, 32, true, false, 163840, true>(g, grid, stream);
+      else
+        go<128, 128, 2, 4, 64, 32, true, false, 163840>(g, grid, stream);
+      break;
     default: go<256, 128, 2, 4, 32, 32, true, false, 163840>(g, grid, stream); break;
   }
   return hipGetLastError();
@@ -51,7 +61,12 @@ static void down(int bm, bool once, const GemmParams& g, unsigned grid, hipStrea
       else
         go<64, 128, 2, 2, 64, 16, false, F32, 81920>(g, grid, stream);
       break;
-    case 128: go<128, 256, 2, 4, 32, 32, false, F32, 163840>(g, grid, stream); break;
+    case 128:
+      if (once)
+        go<128, 256, 2, 4, 64, 32, false, F32, 163840, true>(g, grid, stream);
+      else
+        go<128, 256, 2, 4, 64, 32, false, F32, 163840>(g, grid, stream);
+      break;
     default: go<256, 256, 2, 4, 32, 32, false, F32, 163840>(g, grid, stream); break;
   }
 }

@@ -32,12 +32,17 @@ struct MoeLayout {
   size_t ids, wts, offsets, sorted, pos, tile_map, num_tiles, route_total;
   size_t h, P, expert_total;
   int bm, max_tiles, down_splits, down_kps;
+  // 128-row tiles: experts' rows are expected to fit one tile (average rows
+  // per expert x 1.3 <= 128, the margin pick_bm uses for 32-row tiles), so
+  // each expert's weights are streamed once and load non-temporally.
+  bool once;
 };
 
 static MoeLayout moe_layout(const aflex_ffn_args& f) {
   MoeLayout L;
   const size_t pairs = (size_t)f.T * f.k;
   L.bm = pick_bm((double)pairs / f.E);
+  L.once = L.bm == 128 && (double)pairs / f.E * 1.3 <= 128.0;
   L.max_tiles = (int)((pairs + L.bm - 1) / L.bm) + f.E;
   const int ntiles = (f.H + down_bn(L.bm) - 1) / down_bn(L.bm);
   // The tile count is a worst case here (the routing stays on the device):
@@ -271,7 +276,7 @@ hipError_t launch_moe_experts(const aflex_ffn_args& f, void* route_ws, void* exp
   g.mt_major = 0;  // an expert's m-tiles are adjacent: overflow tiles re-read its weights from L2
   g.C = h;
   g.ldc = f.I;
-  e = launch_gate_up(L.bm, false, g, stream);
+  e = launch_gate_up(L.bm, L.once, g, stream);
   if (e != hipSuccess) return e;
 
   const long long pairs = (long long)f.T * f.k;
@@ -293,7 +298,7 @@ hipError_t launch_moe_experts(const aflex_ffn_args& f, void* route_ws, void* exp
   d.P = P;
   d.p_split_stride = pairs * f.H;
   d.ldp = f.H;
-  e = launch_down(L.bm, true, false, d, stream);
+  e = launch_down(L.bm, true, L.once, d, stream);
   if (e != hipSuccess) return e;
 
   dim3 grid(f.T, (f.H / 4 + 255) / 256);
