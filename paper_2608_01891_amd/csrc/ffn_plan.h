@@ -30,14 +30,14 @@ struct FfnPlan {
 // Rows per m-tile for grouped GEMMs with the given average rows per expert.
 // Up to 32 rows a tile covers a typical expert (its weights are streamed once,
 // non-temporally); up to 48 rows 64-row tiles, two work-groups per CU (an
-// expert's second tile re-reads its weights from L2); up to 160 rows the
-// 8-wave 128-row tile (measured against 64-row tiles: 64 rows per expert
-// 656 -> 620 us, 128 rows 890 -> 830 us; 32 rows 530 -> 600 us, so not
-// there); beyond, the 256-row shape.
+// expert's second tile re-reads its weights from L2; at 32 rows per expert
+// 535 us against 611 us with 128-row tiles); up to 144 rows the 8-wave
+// 128-row tile; beyond, the 256-row shape (Mixtral shapes, 128 rows per
+// expert: 828 us with 128-row tiles, 857 with 256; 160 rows: 936 and 888).
 inline int pick_bm(double rows_per_expert) {
   if (rows_per_expert * 1.3 <= 32) return 32;
   if (rows_per_expert <= 48) return 64;
-  if (rows_per_expert <= 160) return 128;
+  if (rows_per_expert <= 144) return 128;
   return 256;
 }
 

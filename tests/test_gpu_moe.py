@@ -103,10 +103,12 @@ def test_routing_extremes(gpu_lib, T, E, k):
     check_rows(y.cpu(), ref, what=f"moe extremes T={T} E={E} k={k}")
 
 
-@pytest.mark.parametrize("T", [20, 160, 600])
+@pytest.mark.parametrize("T", [20, 160, 200, 384, 448, 576, 584, 600])
 def test_tile_shape_boundaries(gpu_lib, T):
-    """Row counts per expert on both sides of the tile-size thresholds (32-, 64-
-    and 256-row tiles) with 8 experts and top-2."""
+    """Average rows per expert on both sides of the tile-size thresholds with 8
+    experts and top-2: 32-row tiles (5), 64-row (40), 128-row with
+    non-temporal weights (50, 96), 128-row re-reading weights (112, 144) and
+    256-row tiles (146, 150)."""
     x, w, logits = synth.custom_ffn(90 + T, T, 256, 192, E=8)
     y = aflex.moe_ffn(x.to(DEV), w.to(DEV), logits.to(DEV), 2).cpu()
     ref, _, _ = oracle.moe_ffn(x, logits, w.w_gate, w.w_up, w.w_down, 2)
