@@ -5,7 +5,7 @@
 // B [N, K] holds weights in the [out_features, in_features] layout, so both
 // operands have the contraction index contiguous and every MFMA operand is
 // one 16-byte LDS read. Tiles of BM x BN x 64 stream from HBM straight into a
-// ring of 3-4 LDS stages (global_load_lds_dwordx4, no register staging), so
+// ring of 2-4 LDS stages (global_load_lds_dwordx4, no register staging), so
 // the loads of the next k-steps are in flight while kt is multiplied
 // (v_mfma_f32_16x16x32_bf16). At decode batch sizes these GEMMs stream
 // weights, so the depth of the load pipeline, not the MFMA rate, sets their

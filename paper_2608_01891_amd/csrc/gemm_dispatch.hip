@@ -4,10 +4,12 @@
 // waves, 16x16x32 MFMA, 64-wide k-steps, two work-groups per CU, HBM-bound);
 // 128- and 256-row tiles are the 8-wave 32x32x16 MFMA shapes (wave tiles of
 // 64 or 128 rows by 32 columns of each gate/up matrix or 64 columns of the
-// down matrix, one work-group per CU in the whole 160 KiB of LDS). The
-// 128-row tiles take 64-wide k-steps (a ring of three stages), so every
-// k-step reads whole 128-byte lines of each weight row; the 256-row tiles
-// need 32-wide k-steps for a five-stage ring. Weights that one tile streams
+// down matrix, one work-group per CU in the whole 160 KiB of LDS). Both take
+// 64-wide k-steps, so every k-step reads whole 128-byte lines of each row: a
+// ring of three stages for the 128-row tiles, two (the next k-step loads
+// while the current one is multiplied) for the 256-row tiles, which was
+// faster than five stages of 32-wide k-steps (dense T = 512: 474 -> 432 us,
+// T = 4096: 3.02 -> 2.82 ms). Weights that one tile streams
 // exactly once load non-temporally: always for 32-row tiles, for 64- and
 // 128-row tiles when the caller has a single row tile per weight matrix
 // (measured on the 128-row tiles, dense T = 128: 215 -> 188 us for the
@@ -46,7 +48,7 @@ hipError_t launch_gate_up(int bm, bool once, const GemmParams& g, hipStream_t st
       else
         go<128, 128, 2, 4, 64, 32, true, false, 163840>(g, grid, stream);
       break;
-    default: go<256, 128, 2, 4, 32, 32, true, false, 163840>(g, grid, stream); break;
+    default: go<256, 128, 2, 4, 64, 32, true, false, 163840>(g, grid, stream); break;
   }
   return hipGetLastError();
 }
@@ -67,7 +69,7 @@ static void down(int bm, bool once, const GemmParams& g, unsigned grid, hipStrea
       else
         go<128, 256, 2, 4, 64, 32, false, F32, 163840>(g, grid, stream);
       break;
-    default: go<256, 256, 2, 4, 32, 32, false, F32, 163840>(g, grid, stream); break;
+    default: go<256, 256, 2, 4, 64, 32, false, F32, 163840>(g, grid, stream); break;
   }
 }
 
