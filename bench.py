@@ -233,6 +233,31 @@ def main():
     gate_avg_bytes = sum(gate_bytes) / len(gate_bytes)
     achieved = gate_avg_bytes / (avg_ms * 1e-3)
 
+    # The same kernel at the same shapes with nothing else on the GPU: each
+    # microbatch's FFN alone on one stream (what sharing HBM with the
+    # attention stream costs the dominant kernel inside the step).
+    alone_ws = aflex.Workspace()
+    alone_y = torch.empty_like(y)
+
+    def ffn_alone():
+        o = 0
+        for n in mbs:
+            aflex.moe_ffn(y[o:o + n], f, logits[o:o + n], k, y=alone_y[o:o + n], ws=alone_ws)
+            o += n
+
+    ffn_alone()
+    torch.cuda.synchronize()
+    aflex.profile_start([DOMINANT])
+    for _ in range(max(3, args.steps // 4)):
+        ffn_alone()
+    torch.cuda.synchronize()
+    alone = aflex.profile_stop()[DOMINANT]
+    alone_ms = alone[1] / alone[0]
+    standalone = {"avg_launch_ms": round(alone_ms, 5),
+                  "achieved": round(gate_avg_bytes / (alone_ms * 1e-3) / 1e9, 1),
+                  "frac": round(gate_avg_bytes / (alone_ms * 1e-3) / PEAK_HBM, 4),
+                  "note": "same kernel and microbatch shapes, each microbatch's FFN alone on one stream"}
+
     traffic = None
     if os.path.exists(TRAFFIC_FILE):
         with open(TRAFFIC_FILE) as fh:
@@ -266,7 +291,7 @@ def main():
                      "avg_launch_ms": round(avg_ms, 5), "launches": n_launch,
                      "min_launch_ms": round(mn_ms, 5), "max_launch_ms": round(mx_ms, 5),
                      "ms_per_step_with_events": round(ms_step_ev, 4),
-                     "kernel_hash": kernel_hash()},
+                     "kernel_hash": kernel_hash(), "standalone": standalone},
     }
     result["kernels_in_step"] = {kname: {"launches": v[0], "avg_ms": round(v[1] / v[0], 5)}
                                  for kname, v in prof.items()}
