@@ -308,7 +308,7 @@ aflex_status aflex_attn_decode(const aflex_attn_args* a, void* ws, size_t ws_byt
   if (s != AFLEX_OK) return s;
   s = check_ws(ws, ws_bytes, aflex::attn_workspace_bytes(*a), "attn");
   if (s != AFLEX_OK) return s;
-  return hip_status(aflex::launch_attn_decode(*a, ws, (hipStream_t)stream), "attn");
+  return hip_status(aflex::launch_attn_decode(*a, ws, (hipStream_t)stream, true), "attn");
 }
 
 aflex_status aflex_ffn_swiglu_workspace(const aflex_ffn_args* f, size_t* bytes) {
@@ -441,7 +441,7 @@ aflex_status aflex_af_pipeline_step(const aflex_attn_args* a, const aflex_ffn_ar
       aflex_attn_args am = mb_attn(*a, off, n);
       if (l > 0) am.q = f->y + (size_t)off * H;
       am.out = attn_out + (size_t)off * H;
-      if ((e = aflex::launch_attn_decode(am, attn_ws, sa)) != hipSuccess) return hip_status(e, "pipeline: attn");
+      if ((e = aflex::launch_attn_decode(am, attn_ws, sa, false)) != hipSuccess) return hip_status(e, "pipeline: attn");
       if ((e = hipEventRecord(evA[i], sa)) != hipSuccess) return hip_status(e, "pipeline");
       if ((e = hipStreamWaitEvent(sf, evA[i], 0)) != hipSuccess) return hip_status(e, "pipeline");
       aflex_ffn_args fm = mb_ffn(*f, off, n);

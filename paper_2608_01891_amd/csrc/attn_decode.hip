@@ -56,7 +56,18 @@ __device__ __forceinline__ int clamp_ctx(const AttnParams& p, int b) {
   return c < 0 ? 0 : (c > p.max_ctx ? p.max_ctx : c);
 }
 
-template <int D>
+// K/V tile loads; NT marks them non-temporal (each cached byte is read once).
+template <bool NT>
+__device__ __forceinline__ bf16x8 ld_kv(const uint16_t* ptr) {
+  if constexpr (NT) {
+    typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+    return __builtin_bit_cast(bf16x8, __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(ptr)));
+  } else {
+    return ld_bf16x8(ptr);
+  }
+}
+
+template <int D, bool NT>
 __global__ __launch_bounds__(256, 2) void attn_split_kernel(AttnParams p) {
   constexpr int NC = D / 32;   // k-chunks of the QK product
   constexpr int NMT = D / 16;  // d-tiles of the PV product
@@ -130,8 +141,8 @@ __global__ __launch_bounds__(256, 2) void attn_split_kernel(AttnParams p) {
       const uint16_t* kb = p.kc + ((size_t)pk * p.Hkv + kvh) * 16 * D + qg * 8;
 #pragma unroll
       for (int c = 0; c < NC; ++c) {
-        k1[c] = ld_bf16x8(kb + ktok * D + c * 32);
-        k2[c] = ld_bf16x8(kb + (ktok + 4) * D + c * 32);
+        k1[c] = ld_kv<NT>(kb + ktok * D + c * 32);
+        k2[c] = ld_kv<NT>(kb + (ktok + 4) * D + c * 32);
       }
     } else {
 #pragma unroll
@@ -143,7 +154,7 @@ __global__ __launch_bounds__(256, 2) void attn_split_kernel(AttnParams p) {
     if (pv >= 0) {
       const uint16_t* vb = p.vc + ((size_t)pv * p.Hkv + kvh) * D * 16 + vtok;
 #pragma unroll
-      for (int mt = 0; mt < NMT; ++mt) vf[mt] = ld_bf16x8(vb + (mt * 16 + r) * 16);
+      for (int mt = 0; mt < NMT; ++mt) vf[mt] = ld_kv<NT>(vb + (mt * 16 + r) * 16);
     } else {
 #pragma unroll
       for (int mt = 0; mt < NMT; ++mt) vf[mt] = zero_bf16x8();
@@ -313,7 +324,7 @@ size_t attn_workspace_bytes(const aflex_attn_args& a) {
   return align_up(rows * a.D * sizeof(float), 256) + align_up(rows * 2 * sizeof(float), 256);
 }
 
-hipError_t launch_attn_decode(const aflex_attn_args& a, void* ws, hipStream_t stream) {
+hipError_t launch_attn_decode(const aflex_attn_args& a, void* ws, hipStream_t stream, bool nt_kv) {
   AttnParams p;
   p.q = a.q;
   p.kc = a.k_cache;
@@ -340,10 +351,17 @@ hipError_t launch_attn_decode(const aflex_attn_args& a, void* ws, hipStream_t st
   const unsigned merge_grid = (a.B * a.Hq + kWaves - 1) / kWaves;
   {
     ProfScope ps("attn_split", stream);
-    if (a.D == 128)
-      attn_split_kernel<128><<<grid, 256, 0, stream>>>(p);
-    else
-      attn_split_kernel<64><<<grid, 256, 0, stream>>>(p);
+    if (a.D == 128) {
+      if (nt_kv)
+        attn_split_kernel<128, true><<<grid, 256, 0, stream>>>(p);
+      else
+        attn_split_kernel<128, false><<<grid, 256, 0, stream>>>(p);
+    } else {
+      if (nt_kv)
+        attn_split_kernel<64, true><<<grid, 256, 0, stream>>>(p);
+      else
+        attn_split_kernel<64, false><<<grid, 256, 0, stream>>>(p);
+    }
   }
   if (p.max_splits > 1) {
     ProfScope ps("attn_merge", stream);

@@ -12,7 +12,11 @@ inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 // Decode attention (attn_decode.hip).
 int attn_split_tokens(const aflex_attn_args& a);
 size_t attn_workspace_bytes(const aflex_attn_args& a);
-hipError_t launch_attn_decode(const aflex_attn_args& a, void* ws, hipStream_t stream);
+// nt_kv: stream the K/V tiles with non-temporal loads. Decode attention on its
+// own (an attention pool) reads each cached byte once and measured 2-4% faster
+// that way; next to the FFN's weight stream on the same GPU (the two-stream
+// pipeline) ordinary loads measured ~1% faster.
+hipError_t launch_attn_decode(const aflex_attn_args& a, void* ws, hipStream_t stream, bool nt_kv);
 
 // Dense SwiGLU FFN (ffn.hip).
 size_t swiglu_workspace_bytes(const aflex_ffn_args& f);
