@@ -441,7 +441,11 @@ aflex_status aflex_af_pipeline_step(const aflex_attn_args* a, const aflex_ffn_ar
       aflex_attn_args am = mb_attn(*a, off, n);
       if (l > 0) am.q = f->y + (size_t)off * H;
       am.out = attn_out + (size_t)off * H;
-      if ((e = aflex::launch_attn_decode(am, attn_ws, sa, false)) != hipSuccess) return hip_status(e, "pipeline: attn");
+      // The first attention runs before any FFN work (only the routing
+      // overlaps it): non-temporal K/V loads as for attention on its own;
+      // the others share HBM and caches with an FFN weight stream.
+      const bool alone = l == 0 && i == 0;
+      if ((e = aflex::launch_attn_decode(am, attn_ws, sa, alone)) != hipSuccess) return hip_status(e, "pipeline: attn");
       if ((e = hipEventRecord(evA[i], sa)) != hipSuccess) return hip_status(e, "pipeline");
       if ((e = hipStreamWaitEvent(sf, evA[i], 0)) != hipSuccess) return hip_status(e, "pipeline");
       aflex_ffn_args fm = mb_ffn(*f, off, n);
