@@ -674,11 +674,31 @@ def main():
                 break
             n_seq = min(B, max(n_seq + 1, int(n_seq * 15.0 / max(dt, 1e-3))))
             dt, ntok = oracle_sample(n_seq)
+        # The oracle on two more workloads, at one thread and at all of them:
+        # the tiny layer (attention and SwiGLU) and the Qwen3-32B decode attention.
+        nthreads = torch.get_num_threads()
+        wt = synth.tiny_layer()
+        wq = synth.qwen3_attention(device=dev).attn.to("cpu")
+        per_config = {}
+        for threads in (1, nthreads):
+            torch.set_num_threads(threads)
+            ta = wt.attn
+            t0 = time.perf_counter()
+            oracle.attention_decode(ta.q, ta.k_cache, ta.v_cache, ta.block_table, ta.context_lens)
+            oracle.swiglu_ffn(wt.x, wt.ffn.w_gate, wt.ffn.w_up, wt.ffn.w_down)
+            t1 = time.perf_counter()
+            oracle.attention_decode(wq.q, wq.k_cache, wq.v_cache, wq.block_table, wq.context_lens)
+            t2 = time.perf_counter()
+            per_config.setdefault("tiny_layer_attention_and_swiglu_ms", {})[f"{threads}_threads"] = round((t1 - t0) * 1e3, 2)
+            per_config.setdefault("qwen3_attention_B64_ms", {})[f"{threads}_threads"] = round((t2 - t1) * 1e3, 1)
+        torch.set_num_threads(nthreads)
+        del wq
         result["cpu_baseline"] = {
-            "value": round(n_seq / dt, 4), "unit": "tok/s", "cores": torch.get_num_threads(),
+            "value": round(n_seq / dt, 4), "unit": "tok/s", "cores": nthreads,
             "kind": "oracle",
             "sample": f"first {n_seq} of the 256 sequences of the pipeline workload ({ntok} cached "
-                      f"tokens): their attention and top-2 MoE FFN in the float64 oracle, {dt:.1f} s"}
+                      f"tokens): their attention and top-2 MoE FFN in the float64 oracle, {dt:.1f} s",
+            "per_config": per_config}
 
     print(json.dumps(result))
 
