@@ -24,12 +24,15 @@ namespace aflex {
 
 constexpr int kMaxK = 8;
 constexpr int kMaxE = 64;
+// Up to this many tokens one work-group routes the batch (a single launch);
+// larger batches take three kernels that spread the tokens over work-groups.
+constexpr int kSingleRouteMaxT = 512;
 
 // Workspace: a routing block (ids .. num_tiles, written by the route kernel)
 // followed by the expert block (h, P). The two can live apart: the pipeline
 // keeps one routing block per microbatch and one shared expert block.
 struct MoeLayout {
-  size_t ids, wts, offsets, sorted, pos, tile_map, num_tiles, route_total;
+  size_t ids, wts, offsets, sorted, pos, tile_map, num_tiles, blockcnt, blockbase, route_total;
   size_t h, P, expert_total;
   int bm, max_tiles, down_splits, down_kps;
   // 128-row tiles: experts' rows are expected to fit one tile (average rows
@@ -62,6 +65,9 @@ static MoeLayout moe_layout(const aflex_ffn_args& f) {
   L.pos = take(pairs * 4);
   L.tile_map = take((size_t)L.max_tiles * 3 * 4);
   L.num_tiles = take(4);
+  const size_t nblk = ((size_t)f.T + 255) / 256;
+  L.blockcnt = take(nblk * f.E * 4);
+  L.blockbase = take(nblk * f.E * 4);
   L.route_total = o;
   o = 0;
   L.h = take(pairs * f.I * 2);
@@ -75,6 +81,70 @@ size_t moe_expert_bytes(const aflex_ffn_args& f) { return moe_layout(f).expert_t
 size_t moe_workspace_bytes(const aflex_ffn_args& f) {
   const MoeLayout L = moe_layout(f);
   return L.route_total + L.expert_total;
+}
+
+// Top-k of one token's logits (descending, ties to the lower id) and the
+// softmax over the selected ones.
+__device__ __forceinline__ void topk_token(const float* l, int E, int k, int* sid, float* w) {
+  uint64_t taken = 0;
+  float sel[kMaxK];
+  for (int j = 0; j < k; ++j) {
+    int bi = -1;
+    float bv = 0.f;
+    for (int e = 0; e < E; ++e) {
+      if ((taken >> e) & 1) continue;
+      const float v = l[e];
+      if (bi < 0 || v > bv) {
+        bi = e;
+        bv = v;
+      }
+    }
+    taken |= 1ull << bi;
+    sel[j] = bv;
+    sid[j] = bi;
+  }
+  float z = 0.f, ex[kMaxK];
+  for (int j = 0; j < k; ++j) {
+    ex[j] = expf(sel[j] - sel[0]);
+    z += ex[j];
+  }
+  for (int j = 0; j < k; ++j) w[j] = ex[j] / z;
+}
+
+// m-tiles of bm rows per expert, in expert order (one thread).
+__device__ __forceinline__ void build_tile_map(const int* off, int E, int bm, int32_t* tile_map, int32_t* num_tiles) {
+  int nt = 0;
+  for (int e = 0; e < E; ++e)
+    for (int r = off[e]; r < off[e + 1]; r += bm) {
+      tile_map[3 * nt + 0] = e;
+      tile_map[3 * nt + 1] = r;
+      tile_map[3 * nt + 2] = min(r + bm, off[e + 1]);
+      ++nt;
+    }
+  *num_tiles = nt;
+}
+
+// Stable rank of each of a 256-token chunk's pairs among the chunk's pairs of
+// the same expert (token order, i.e. wave by wave, lane by lane): pre[j] within
+// the wave, wcnt[w][e] the pairs of expert e in wave w.
+__device__ __forceinline__ void chunk_ranks(const int* my_e, bool valid, int E, int k, int wave, int lane, int* pre,
+                                            int (*wcnt)[kMaxE]) {
+  const uint64_t lt = (1ull << lane) - 1ull;
+  uint64_t mask = 0;
+  for (int j = 0; j < k; ++j) {
+    pre[j] = 0;
+    if (valid) mask |= 1ull << my_e[j];
+  }
+  for (int e = 0; e < E; ++e) {
+    const bool f = (mask >> e) & 1ull;
+    const uint64_t bal = __ballot(f);
+    if (f) {
+      const int pr = __popcll(bal & lt);
+      for (int j = 0; j < k; ++j)
+        if (my_e[j] == e) pre[j] = pr;
+    }
+    if (lane == 0) wcnt[wave][e] = __popcll(bal);
+  }
 }
 
 __global__ __launch_bounds__(256) void moe_route_kernel(const float* __restrict__ logits, int T, int E, int k,
@@ -95,36 +165,14 @@ __global__ __launch_bounds__(256) void moe_route_kernel(const float* __restrict_
 
   // 1. top-k and softmax over the selected logits.
   for (int t = tid; t < T; t += 256) {
-    const float* l = logits + (size_t)t * E;
-    uint64_t taken = 0;
-    float sel[kMaxK];
     int sid[kMaxK];
+    float w[kMaxK];
+    topk_token(logits + (size_t)t * E, E, k, sid, w);
     for (int j = 0; j < k; ++j) {
-      int bi = -1;
-      float bv = 0.f;
-      for (int e = 0; e < E; ++e) {
-        if ((taken >> e) & 1) continue;
-        const float v = l[e];
-        if (bi < 0 || v > bv) {
-          bi = e;
-          bv = v;
-        }
-      }
-      taken |= 1ull << bi;
-      sel[j] = bv;
-      sid[j] = bi;
-    }
-    float z = 0.f, ex[kMaxK];
-    for (int j = 0; j < k; ++j) {
-      ex[j] = expf(sel[j] - sel[0]);
-      z += ex[j];
-    }
-    for (int j = 0; j < k; ++j) {
-      const float w = ex[j] / z;
       ids[t * k + j] = sid[j];
-      wts[t * k + j] = w;
+      wts[t * k + j] = w[j];
       if (u_ids) u_ids[t * k + j] = sid[j];
-      if (u_w) u_w[t * k + j] = w;
+      if (u_w) u_w[t * k + j] = w[j];
       atomicAdd(&cnt[sid[j]], 1);
     }
   }
@@ -134,15 +182,7 @@ __global__ __launch_bounds__(256) void moe_route_kernel(const float* __restrict_
   if (tid == 0) {
     off[0] = 0;
     for (int e = 0; e < E; ++e) off[e + 1] = off[e] + cnt[e];
-    int nt = 0;
-    for (int e = 0; e < E; ++e)
-      for (int r = off[e]; r < off[e + 1]; r += bm) {
-        tile_map[3 * nt + 0] = e;
-        tile_map[3 * nt + 1] = r;
-        tile_map[3 * nt + 2] = min(r + bm, off[e + 1]);
-        ++nt;
-      }
-    *num_tiles = nt;
+    build_tile_map(off, E, bm, tile_map, num_tiles);
   }
   __syncthreads();
   if (tid <= E) {
@@ -152,27 +192,12 @@ __global__ __launch_bounds__(256) void moe_route_kernel(const float* __restrict_
 
   // 3. stable ranks: pairs of expert e are ordered by token (a token holds e
   //    at most once), chunk by chunk of 256 tokens, wave by wave, lane by lane.
-  const uint64_t lt = (1ull << lane) - 1ull;
   for (int c0 = 0; c0 < T; c0 += 256) {
     const int t = c0 + tid;
     const bool valid = t < T;
     int my_e[kMaxK], pre[kMaxK];
-    uint64_t mask = 0;
-    for (int j = 0; j < k; ++j) {
-      my_e[j] = valid ? ids[t * k + j] : -1;
-      pre[j] = 0;
-      if (valid) mask |= 1ull << my_e[j];
-    }
-    for (int e = 0; e < E; ++e) {
-      const bool f = (mask >> e) & 1ull;
-      const uint64_t bal = __ballot(f);
-      if (f) {
-        const int pr = __popcll(bal & lt);
-        for (int j = 0; j < k; ++j)
-          if (my_e[j] == e) pre[j] = pr;
-      }
-      if (lane == 0) wcnt[wave][e] = __popcll(bal);
-    }
+    for (int j = 0; j < k; ++j) my_e[j] = valid ? ids[t * k + j] : -1;
+    chunk_ranks(my_e, valid, E, k, wave, lane, pre, wcnt);
     __syncthreads();
     if (valid) {
       for (int j = 0; j < k; ++j) {
@@ -188,6 +213,88 @@ __global__ __launch_bounds__(256) void moe_route_kernel(const float* __restrict_
     __syncthreads();
     if (tid < E) base[tid] += wcnt[0][tid] + wcnt[1][tid] + wcnt[2][tid] + wcnt[3][tid];
     __syncthreads();
+  }
+}
+
+// The same routing for larger batches in three kernels, so that the per-token
+// work is spread over one work-group per 256 tokens instead of looping in one:
+// (1) top-k and the chunk's expert counts, (2) offsets, tile map and each
+// chunk's first rank per expert, (3) the chunk's stable ranks. The pair order
+// is the single kernel's.
+__global__ __launch_bounds__(256) void moe_topk_kernel(const float* __restrict__ logits, int T, int E, int k,
+                                                       int32_t* ids, float* wts, int32_t* u_ids, float* u_w,
+                                                       int32_t* blockcnt) {
+  __shared__ int cnt[kMaxE];
+  const int tid = threadIdx.x;
+  if (tid < kMaxE) cnt[tid] = 0;
+  __syncthreads();
+  const int t = blockIdx.x * 256 + tid;
+  if (t < T) {
+    int sid[kMaxK];
+    float w[kMaxK];
+    topk_token(logits + (size_t)t * E, E, k, sid, w);
+    for (int j = 0; j < k; ++j) {
+      ids[t * k + j] = sid[j];
+      wts[t * k + j] = w[j];
+      if (u_ids) u_ids[t * k + j] = sid[j];
+      if (u_w) u_w[t * k + j] = w[j];
+      atomicAdd(&cnt[sid[j]], 1);
+    }
+  }
+  __syncthreads();
+  if (tid < E) blockcnt[(size_t)blockIdx.x * E + tid] = cnt[tid];
+}
+
+__global__ __launch_bounds__(256) void moe_offsets_kernel(const int32_t* __restrict__ blockcnt, int nblk, int E,
+                                                          int bm, int32_t* offsets, int32_t* u_offsets,
+                                                          int32_t* tile_map, int32_t* num_tiles,
+                                                          int32_t* blockbase) {
+  __shared__ int tot[kMaxE];
+  __shared__ int off[kMaxE + 1];
+  const int tid = threadIdx.x;
+  if (tid < E) {
+    int sum = 0;
+    for (int b = 0; b < nblk; ++b) {
+      blockbase[(size_t)b * E + tid] = sum;
+      sum += blockcnt[(size_t)b * E + tid];
+    }
+    tot[tid] = sum;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    off[0] = 0;
+    for (int e = 0; e < E; ++e) off[e + 1] = off[e] + tot[e];
+    build_tile_map(off, E, bm, tile_map, num_tiles);
+  }
+  __syncthreads();
+  if (tid <= E) {
+    offsets[tid] = off[tid];
+    if (u_offsets) u_offsets[tid] = off[tid];
+  }
+}
+
+__global__ __launch_bounds__(256) void moe_rank_kernel(const int32_t* __restrict__ ids, int T, int E, int k,
+                                                       const int32_t* __restrict__ offsets,
+                                                       const int32_t* __restrict__ blockbase, int32_t* sorted,
+                                                       int32_t* pos, int32_t* u_sorted) {
+  __shared__ int wcnt[4][kMaxE];
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int t = blockIdx.x * 256 + tid;
+  const bool valid = t < T;
+  int my_e[kMaxK], pre[kMaxK];
+  for (int j = 0; j < k; ++j) my_e[j] = valid ? ids[t * k + j] : -1;
+  chunk_ranks(my_e, valid, E, k, wave, lane, pre, wcnt);
+  __syncthreads();
+  if (valid) {
+    for (int j = 0; j < k; ++j) {
+      const int e = my_e[j];
+      int r = blockbase[(size_t)blockIdx.x * E + e] + pre[j];
+      for (int w = 0; w < wave; ++w) r += wcnt[w][e];
+      const int pidx = offsets[e] + r;
+      sorted[pidx] = t * k + j;
+      pos[t * k + j] = pidx;
+      if (u_sorted) u_sorted[pidx] = t * k + j;
+    }
   }
 }
 
@@ -225,13 +332,29 @@ __global__ __launch_bounds__(256) void moe_combine_kernel(const float* __restric
 hipError_t launch_moe_route(const aflex_ffn_args& f, void* route_ws, hipStream_t stream) {
   const MoeLayout L = moe_layout(f);
   char* w = static_cast<char*>(route_ws);
+  int32_t* ids = reinterpret_cast<int32_t*>(w + L.ids);
+  float* wts = reinterpret_cast<float*>(w + L.wts);
+  int32_t* offsets = reinterpret_cast<int32_t*>(w + L.offsets);
+  int32_t* sorted = reinterpret_cast<int32_t*>(w + L.sorted);
+  int32_t* pos = reinterpret_cast<int32_t*>(w + L.pos);
+  int32_t* tile_map = reinterpret_cast<int32_t*>(w + L.tile_map);
+  int32_t* num_tiles = reinterpret_cast<int32_t*>(w + L.num_tiles);
   ProfScope ps("moe_route", stream);
-  moe_route_kernel<<<1, 256, 0, stream>>>(
-      f.router_logits, f.T, f.E, f.k, L.bm, reinterpret_cast<int32_t*>(w + L.ids),
-      reinterpret_cast<float*>(w + L.wts), reinterpret_cast<int32_t*>(w + L.offsets),
-      reinterpret_cast<int32_t*>(w + L.sorted), reinterpret_cast<int32_t*>(w + L.pos),
-      reinterpret_cast<int32_t*>(w + L.tile_map), reinterpret_cast<int32_t*>(w + L.num_tiles), f.topk_ids,
-      f.topk_w, f.expert_offsets, f.sorted_pairs);
+  if (f.T <= kSingleRouteMaxT) {
+    moe_route_kernel<<<1, 256, 0, stream>>>(f.router_logits, f.T, f.E, f.k, L.bm, ids, wts, offsets, sorted, pos,
+                                            tile_map, num_tiles, f.topk_ids, f.topk_w, f.expert_offsets,
+                                            f.sorted_pairs);
+    return hipGetLastError();
+  }
+  const int nblk = (f.T + 255) / 256;
+  int32_t* blockcnt = reinterpret_cast<int32_t*>(w + L.blockcnt);
+  int32_t* blockbase = reinterpret_cast<int32_t*>(w + L.blockbase);
+  moe_topk_kernel<<<nblk, 256, 0, stream>>>(f.router_logits, f.T, f.E, f.k, ids, wts, f.topk_ids, f.topk_w,
+                                            blockcnt);
+  moe_offsets_kernel<<<1, 256, 0, stream>>>(blockcnt, nblk, f.E, L.bm, offsets, f.expert_offsets, tile_map,
+                                            num_tiles, blockbase);
+  moe_rank_kernel<<<nblk, 256, 0, stream>>>(ids, f.T, f.E, f.k, offsets, blockbase, sorted, pos,
+                                            f.sorted_pairs);
   return hipGetLastError();
 }
 

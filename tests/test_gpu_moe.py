@@ -91,10 +91,13 @@ def test_mixtral_prefill_tokens_sampled(gpu_lib, mixtral):
     check_rows(y.cpu()[toks], ref[toks], what="mixtral moe prefill T=4096 (sampled)")
 
 
-@pytest.mark.parametrize("T,E,k", [(200, 64, 8), (33, 64, 1), (64, 2, 2)])
+@pytest.mark.parametrize("T,E,k", [(200, 64, 8), (33, 64, 1), (64, 2, 2), (512, 8, 2), (513, 8, 2),
+                                   (1025, 3, 3), (1500, 64, 8), (2000, 64, 1)])
 def test_routing_extremes(gpu_lib, T, E, k):
     """The largest supported expert count and top-k (E = 64, k = 8), top-1 over
-    64 experts (many empty experts), and k = E."""
+    64 experts (many empty experts), and k = E; on both sides of the batch size
+    where routing moves from one work-group to one per 256 tokens (512), with
+    ragged last chunks."""
     H, I = 128, 128
     x, w, logits = synth.custom_ffn(80 + E + k, T, H, I, E=E)
     y, r = aflex.moe_ffn(x.to(DEV), w.to(DEV), logits.to(DEV), k, routing=True)
