@@ -35,9 +35,11 @@ struct MoeLayout {
   size_t ids, wts, offsets, sorted, pos, tile_map, num_tiles, blockcnt, blockbase, route_total;
   size_t h, P, expert_total;
   int bm, max_tiles, down_splits, down_kps;
-  // 128-row tiles: experts' rows are expected to fit one tile (average rows
-  // per expert x 1.3 <= 128, the margin pick_bm uses for 32-row tiles), so
-  // each expert's weights are streamed once and load non-temporally.
+  // 64- and 128-row tiles: experts' rows are expected to fit one tile
+  // (average rows per expert x 1.3 <= bm, the margin pick_bm uses for 32-row
+  // tiles), so each expert's weights are streamed once and load
+  // non-temporally (measured 4-5% faster at 32-48 rows per expert on 64-row
+  // tiles, 11% at 64 rows per expert on 128-row tiles).
   bool once;
 };
 
@@ -45,7 +47,7 @@ static MoeLayout moe_layout(const aflex_ffn_args& f) {
   MoeLayout L;
   const size_t pairs = (size_t)f.T * f.k;
   L.bm = pick_bm((double)pairs / f.E);
-  L.once = L.bm == 128 && (double)pairs / f.E * 1.3 <= 128.0;
+  L.once = (L.bm == 64 || L.bm == 128) && (double)pairs / f.E * 1.3 <= (double)L.bm;
   L.max_tiles = (int)((pairs + L.bm - 1) / L.bm) + f.E;
   const int ntiles = (f.H + down_bn(L.bm) - 1) / down_bn(L.bm);
   // The tile count is a worst case here (the routing stays on the device):
