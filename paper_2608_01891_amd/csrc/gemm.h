@@ -7,7 +7,8 @@
 // one 16-byte LDS read. Tiles of BM x BN x 64 stream from HBM straight into a
 // ring of 2-4 LDS stages (global_load_lds_dwordx4, no register staging), so
 // the loads of the next k-steps are in flight while kt is multiplied
-// (v_mfma_f32_16x16x32_bf16). At decode batch sizes these GEMMs stream
+// (v_mfma_f32_16x16x32_bf16 for the 32/64-row tiles, v_mfma_f32_32x32x16_bf16
+// for the 128/256-row ones). At decode batch sizes these GEMMs stream
 // weights, so the depth of the load pipeline, not the MFMA rate, sets their
 // speed.
 //

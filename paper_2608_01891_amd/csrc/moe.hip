@@ -8,8 +8,9 @@
 //      softmax over the k selected logits; per-expert counts, their exclusive
 //      prefix, the stable (expert, token, slot) order of the token/slot pairs,
 //      each pair's position in that order, and the m-tile map of the grouped
-//      GEMMs. One work-group; ranks come from wave ballots, so the order is
-//      deterministic.
+//      GEMMs. One work-group up to 512 tokens, else three kernels over chunks
+//      of 256 tokens; ranks come from wave ballots, so the order is
+//      deterministic (and the same for both paths).
 //   2. grouped gate/up GEMM with fused SwiGLU; the A rows are gathered from x
 //      through the pair order (no permuted copy of x is written).
 //   3. grouped down GEMM into fp32 split-K partials, rows in pair order.
