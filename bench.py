@@ -18,6 +18,7 @@ import argparse
 import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -33,11 +34,21 @@ TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gemm_gate_up_af_pipeline_traffic.
 KERNEL_SOURCES = ["gemm.h", "gemm_dispatch.hip", "ffn_plan.h", "moe.hip"]
 
 
+def _code_only(text):
+    """C++ source without comments and whitespace, so that a comment edit does
+    not mark the stored counter readings as stale."""
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    text = re.sub(r"//[^\n]*", "", text)
+    return re.sub(r"\s+", "", text)
+
+
 def kernel_hash():
+    """Hash of the dominant kernel's sources (code only), recorded with the
+    counter readings in TRAFFIC_FILE."""
     h = hashlib.sha256()
     for f in KERNEL_SOURCES:
-        with open(os.path.join(ROOT, "paper_2608_01891_amd", "csrc", f), "rb") as fh:
-            h.update(fh.read())
+        with open(os.path.join(ROOT, "paper_2608_01891_amd", "csrc", f)) as fh:
+            h.update(_code_only(fh.read()).encode())
     return h.hexdigest()[:16]
 
 
