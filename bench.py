@@ -61,6 +61,8 @@ def parse():
     p.add_argument("--no-operators", action="store_true", help="skip the per-operator section")
     p.add_argument("--counters-pass", action="store_true",
                    help="only warm-up + steps of the layer step and a 1 GiB copy (for rocprofv3 --pmc)")
+    p.add_argument("--prefill-counters-pass", action="store_true",
+                   help="only the causal prefill attention at 2 x 4096 Qwen3-32B tokens, for rocprofv3 --pmc")
     p.add_argument("--ffn-counters-pass", action="store_true",
                    help="only the MFMA-bound FFN shapes (Qwen3 SwiGLU T=512, Mixtral MoE T=2048), for rocprofv3 --pmc")
     return p.parse_args()
@@ -157,6 +159,16 @@ def main():
 
     def step(m=mbs):
         aflex.af_pipeline_step(a, f, logits, k, m, y=y, stream_a=sa, stream_f=sf, ws=pws, join=False)
+
+    if args.prefill_counters_pass:
+        pw = synth.prefill_workload("qwen3-32b", 4096, 2, device=dev)
+        outp = aflex.attn_prefill(pw)
+        for _ in range(3):
+            aflex.attn_prefill(pw, out=outp)
+        torch.cuda.synchronize()
+        print("prefill counters pass: 2 x 4096 done", flush=True)
+        print(json.dumps({"prefill_counters_pass": True}))
+        return
 
     if args.ffn_counters_pass:
         # Counter collection for the MFMA-bound FFN GEMMs: a few calls of each shape.
