@@ -29,13 +29,20 @@ CFLAGS = [
 ]
 
 
+# Per-file additions. The causal prefill kernel's softmax is bound by vector-ALU
+# issue; its scores are finite or -inf (masked), never NaN, and without NaN
+# semantics its running maxima need no canonicalising instructions (about 17%
+# fewer VALU instructions per key tile).
+FILE_FLAGS = {"attn_prefill.hip": ["-fno-honor-nans"]}
+
+
 def sources():
     return sorted(os.path.join(CSRC, f) for f in os.listdir(CSRC) if f.endswith(".hip"))
 
 
 def _compile(src: str) -> str:
     obj = os.path.join(BUILD, os.path.basename(src) + ".o")
-    cmd = [HIPCC, *CFLAGS, "-c", src, "-o", obj]
+    cmd = [HIPCC, *CFLAGS, *FILE_FLAGS.get(os.path.basename(src), []), "-c", src, "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"hipcc failed for {src}:\n{r.stderr}")
