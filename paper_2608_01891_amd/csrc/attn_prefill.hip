@@ -22,8 +22,11 @@
 //                   (B operand) stay in registers for the whole kernel.
 //   softmax         online, in the log2 domain: each lane holds 32 scores of
 //                   one query row (an accumulator column), the other 32 sit in
-//                   lane l ^ 32; O and l are rescaled only when a row's maximum
-//                   rises more than 2^8 above the reference maximum.
+//                   lane l ^ 32 (row maxima meet through v_permlane32_swap);
+//                   O and l are rescaled only when a row's maximum rises more
+//                   than 2^8 above the reference maximum. The row sum l adds
+//                   the bf16-rounded weights that enter O (v_dot2 with (1, 1)),
+//                   so numerator and denominator use the same weights.
 //   O^T += V^T P^T  P^T is used straight from the S^T accumulator registers as
 //                   the B operand (rounded to bf16); the V^T fragments (A
 //                   operand) come from the row-major V tile through the
@@ -59,6 +62,7 @@ struct PrefillParams {
 typedef float f32x8 __attribute__((ext_vector_type(8)));
 typedef short s16x4 __attribute__((ext_vector_type(4)));
 typedef short s16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
 __device__ __forceinline__ void wait_vm0() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
@@ -74,6 +78,12 @@ __device__ __forceinline__ uint32_t kv_off(int row, int chunk) { return row * 25
 // i % 4 of the 4-element segment addressed by lane 4 j + i / 4, as element j.
 __device__ __forceinline__ s16x4 lds_read_tr16(const uint8_t* p) {
   return __builtin_amdgcn_ds_read_tr16_b64_v4i16((s16x4 __attribute__((address_space(3)))*)p);
+}
+
+// Maximum of a lane's value and lane l ^ 32's (one v_permlane32_swap).
+__device__ __forceinline__ float max_across_halves(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
 }
 
 __global__ __launch_bounds__(256, 2) void attn_prefill_kernel(PrefillParams p) {
@@ -154,6 +164,9 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_kernel(PrefillParams p) {
 #pragma unroll
     for (int i = 0; i < 16; ++i) oacc[db][i] = 0.f;
   float m_run = kNegInf, l_run = 0.f;
+  float m_thr = kNegInf;  // m_run + 8 / c: a row maximum above it triggers a rescale
+  const float thr_gap = 8.f / p.c;
+  const bf16x2 ones2 = {(__bf16)1.f, (__bf16)1.f};
   f32x16 sc0, sc1, sn0, sn1;  // scores of the current tile and of the next one
 
 #define AFLEX_QK(S0, S1, BUF)                                                                    \
@@ -187,16 +200,17 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_kernel(PrefillParams p) {
           if (key_ + 32 > lim_) SC1[i] = kNegInf;                                            \
         }                                                                                    \
       }                                                                                      \
-      float mx_ = kNegInf;                                                                   \
-      _Pragma("unroll") for (int i = 0; i < 16; ++i) mx_ = fmaxf(mx_, fmaxf(SC0[i], SC1[i])); \
-      mx_ = fmaxf(mx_, __shfl_xor(mx_, 32));                                                 \
-      if (__ballot((mx_ - m_run) * p.c > 8.f) != 0) {                                        \
+      float mx_ = fmaxf(SC0[0], SC1[0]);                                                     \
+      _Pragma("unroll") for (int i = 1; i < 16; ++i) mx_ = fmaxf(fmaxf(mx_, SC0[i]), SC1[i]); \
+      mx_ = max_across_halves(mx_);                                                          \
+      if (__ballot(mx_ > m_thr) != 0) {                                                      \
         const float mnew_ = fmaxf(m_run, mx_);                                               \
         const float alpha_ = fast_exp2((m_run - mnew_) * p.c);                               \
         l_run *= alpha_;                                                                     \
         _Pragma("unroll") for (int db = 0; db < kPD / 32; ++db)                              \
             _Pragma("unroll") for (int i = 0; i < 16; ++i) oacc[db][i] *= alpha_;            \
         m_run = mnew_;                                                                       \
+        m_thr = m_run + thr_gap;                                                             \
       }                                                                                      \
       /* next tile's scores: independent of the exponentials below, which the */             \
       /* scheduler interleaves with them (dropped after a wave's last tile)   */             \
@@ -209,10 +223,13 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_kernel(PrefillParams p) {
         _Pragma("unroll") for (int e = 0; e < 8; ++e) {                                      \
           const float s_ = (ks < 2) ? SC0[(ks & 1) * 8 + e] : SC1[(ks & 1) * 8 + e];         \
           const float pe_ = fast_exp2(__builtin_fmaf(s_, p.c, -mc_));                        \
-          lsum_ += pe_;                                                                      \
           pv_[e] = pe_;                                                                      \
         }                                                                                    \
         pb_[ks] = __builtin_convertvector(pv_, bf16x8);                                      \
+        lsum_ = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pb_[ks], pb_[ks], 0, 1), ones2, lsum_, false); \
+        lsum_ = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pb_[ks], pb_[ks], 2, 3), ones2, lsum_, false); \
+        lsum_ = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pb_[ks], pb_[ks], 4, 5), ones2, lsum_, false); \
+        lsum_ = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pb_[ks], pb_[ks], 6, 7), ones2, lsum_, false); \
       }                                                                                      \
       l_run += lsum_;                                                                        \
       /* O^T += V^T P^T: slot hi*8 + e of k-step ks is key ks*16 + (e/4)*8 + hi*4 + e%4 */    \
