@@ -334,9 +334,17 @@ def main():
     dst = torch.empty_like(src)
     dst.copy_(src)
     ms_copy = timed(lambda: dst.copy_(src), 5)
+    # A read-dominated reference: the vendor BLAS matrix-vector product over the
+    # same 2 GiB viewed as a [262144, 4096] bf16 matrix.
+    mat = src.view(torch.bfloat16).view(-1, 4096)
+    vec = torch.ones(4096, dtype=torch.bfloat16, device=dev)
+    torch.mv(mat, vec)
+    ms_mv = timed(lambda: torch.mv(mat, vec), 5)
     result["hbm_reference"] = {"copy_GB_per_s": round(4 * (1 << 30) / (ms_copy * 1e-3) / 1e9, 1),
-                               "note": "read + write bytes of a 2 GiB device copy / time"}
-    del src, dst
+                               "gemv_read_GB_per_s": round(2 * (1 << 30) / (ms_mv * 1e-3) / 1e9, 1),
+                               "note": "read + write bytes of a 2 GiB device copy / time; bytes of a "
+                                       "2 GiB bf16 matrix read by torch.mv / time"}
+    del src, dst, mat, vec
 
     # ---------------- energy per token (where the counter is readable) -------------
     read_energy = energy_reader()
@@ -716,6 +724,26 @@ def main():
             per_config.setdefault("qwen3_attention_B64_ms", {})[f"{threads}_threads"] = round((t2 - t1) * 1e3, 1)
         torch.set_num_threads(nthreads)
         del wq
+        # The dense SwiGLU (Qwen3-32B weights) at each decode batch size and the
+        # Mixtral MoE at 256 tokens, all threads: wall time and tokens/s.
+        wg = synth.make_ffn_weights(2, 5120, 25600, device=dev)  # generated on the GPU, copied
+        wq3 = synth.FFNWeights(wg.w_gate.cpu(), wg.w_up.cpu(), wg.w_down.cpu(), 5120, 25600, 0)
+        x512c = synth.qwen3_swiglu(512, device=dev, weights=wg).x.cpu()
+        del wg
+        for T in (32, 128, 512):
+            t0 = time.perf_counter()
+            oracle.swiglu_ffn(x512c[:T], wq3.w_gate, wq3.w_up, wq3.w_down)
+            t1 = time.perf_counter()
+            per_config[f"qwen3_swiglu_T{T}"] = {"threads": nthreads, "ms": round((t1 - t0) * 1e3, 1),
+                                               "tok_s": round(T / (t1 - t0), 2)}
+        del wq3, x512c
+        mc = synth.mixtral_moe(T=256, weights=synth.FFNWeights(f.w_gate.cpu(), f.w_up.cpu(), f.w_down.cpu(), H, I, f.E))
+        t0 = time.perf_counter()
+        oracle.moe_ffn(mc.x, mc.router_logits, mc.ffn.w_gate, mc.ffn.w_up, mc.ffn.w_down, 2)
+        t1 = time.perf_counter()
+        per_config["mixtral_moe_T256"] = {"threads": nthreads, "ms": round((t1 - t0) * 1e3, 1),
+                                          "tok_s": round(256 / (t1 - t0), 2)}
+        del mc
         result["cpu_baseline"] = {
             "value": round(n_seq / dt, 4), "unit": "tok/s", "cores": nthreads,
             "kind": "oracle",
