@@ -32,7 +32,7 @@ def qwen3_weights():
     del w
 
 
-@pytest.mark.parametrize("T", [32, 128, 512])
+@pytest.mark.parametrize("T", [32, 128, 256, 512])
 def test_qwen3_shape_sampled(gpu_lib, qwen3_weights, T):
     w, (wg, wu, wd) = qwen3_weights
     wl = synth.qwen3_swiglu(T, device=DEV, weights=w)

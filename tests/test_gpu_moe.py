@@ -78,6 +78,20 @@ def test_mixtral_shape(gpu_lib, mixtral):
     assert torch.equal(y, y2)
 
 
+def test_mixtral_2048_tokens_sampled(gpu_lib, mixtral):
+    """The MoE at 2048 tokens (seed 103), the MFMA-bound decode size timed by the
+    benchmark: 256-row tiles, routing in three kernels."""
+    T = 2048
+    wl = synth.mixtral_moe(device=DEV, T=T, seed=103, weights=mixtral.ffn)
+    y, r = aflex.moe_ffn(wl.x, wl.ffn, wl.router_logits, 2, routing=True)
+    _check_routing(r, wl.router_logits, 2, 8)
+    toks = sample_rows(T, 6, seed=103, must=[0, T - 1])
+    f = wl.ffn
+    ref, _, _ = oracle.moe_ffn(wl.x.cpu(), wl.router_logits.cpu(), f.w_gate.cpu(), f.w_up.cpu(),
+                               f.w_down.cpu(), 2, token_indices=toks)
+    check_rows(y.cpu()[toks], ref[toks], what="mixtral moe T=2048 (sampled)")
+
+
 def test_mixtral_prefill_tokens_sampled(gpu_lib, mixtral):
     """The MoE FFN over a prefill batch (T = 4096 tokens, 8192 token/slot pairs)."""
     T = 4096
