@@ -221,13 +221,14 @@ __global__ __launch_bounds__(64 * WM * WN, LDS_BYTES > 81920 ? 1 : 2) void gemm_
   constexpr int CPS = BK / KC;             // MFMA k-chunks per stage
   const int nchunks = nk * CPS;
 
-  // Fragments of k-chunk C (of stage C / CPS) into registers FA, FB.
-#define AFLEX_GEMM_READ(FA, FB, C)                                                         \
+  // Fragments of k-chunk C (of stage C / CPS) into registers FA (the first
+  // TMA row blocks of the wave) and FB.
+#define AFLEX_GEMM_READ(FA, FB, C, TMA)                                                    \
   do {                                                                                    \
     const int kt_ = (C) / CPS;                                                            \
     const uint16_t* smp_ = sm[kt_ % STAGES];                                              \
     const int ch_ = ((C) - kt_ * CPS) * (KC / 8) + qg;                                    \
-    _Pragma("unroll") for (int i = 0; i < TM; ++i) {                                      \
+    _Pragma("unroll") for (int i = 0; i < (TMA); ++i) {                                   \
       const int R = wm * WTM + i * MS + r;                                                \
       FA[i] = *reinterpret_cast<const bf16x8*>(&smp_[R * BK + ((ch_ ^ ((R / WIN) % CPR)) << 3)]); \
     }                                                                                     \
@@ -237,10 +238,10 @@ __global__ __launch_bounds__(64 * WM * WN, LDS_BYTES > 81920 ? 1 : 2) void gemm_
       FB[nb][j] = *reinterpret_cast<const bf16x8*>(&smp_[R * BK + ((ch_ ^ ((R / WIN) % CPR)) << 3)]); \
     }                                                                                     \
   } while (0)
-#define AFLEX_GEMM_MMA(FA, FB)                                                             \
+#define AFLEX_GEMM_MMA(FA, FB, TMA)                                                        \
   do {                                                                                    \
     _Pragma("unroll") for (int nb = 0; nb < NB; ++nb)                                     \
-        _Pragma("unroll") for (int i = 0; i < TM; ++i)                                    \
+        _Pragma("unroll") for (int i = 0; i < (TMA); ++i)                                 \
             _Pragma("unroll") for (int j = 0; j < TN; ++j) {                              \
       if constexpr (MS == 16)                                                             \
         acc[nb][i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(FA[i], FB[nb][j], acc[nb][i][j], 0, 0, 0); \
@@ -274,43 +275,73 @@ __global__ __launch_bounds__(64 * WM * WN, LDS_BYTES > 81920 ? 1 : 2) void gemm_
   // chunk c+2 re-read the last k-step (clamped), which is never used.
   // Measured against the guarded two-chunk loop (whose waits covered the
   // reads just issued): 4-5% at the MFMA-bound shapes, bit-identical.
-  if (nk > 0) {
-    bf16x8 fa0[TM], fb0[NB][TN], fa1[TM], fb1[NB][TN];
+  // Row blocks of this wave that hold rows of the tile: a partly filled row
+  // tile (an expert's last rows, a dense remainder) multiplies only those.
+  const int nact = (min(max(row1 - row0 - wm * WTM, 0), WTM) + MS - 1) / MS;
+  if (nk > 0 && nact == 0) {
+    // No row of this wave lies in the tile: it multiplies nothing, but still
+    // loads its share of every stage and takes part in the same barriers, so
+    // the MFMA pipe of its SIMD is left to the other wave.
 #pragma unroll
     for (int st = 0; st < STAGES - 1; ++st) AFLEX_GEMM_ISSUE(sm[st], st);
     AFLEX_GEMM_STAGE(0);
-    AFLEX_GEMM_READ(fa0, fb0, 0);
-    static_assert(CPS % 2 == 0, "an even number of MFMA k-chunks per stage");
-    constexpr int NREAD = TM + NB * TN, NMMA = NB * TM * TN;
-    static_assert(NMMA >= NREAD, "interleave pattern");
-#define AFLEX_GEMM_INTERLEAVE()                                              \
-  do {                                                                       \
-    _Pragma("unroll") for (int i_ = 0; i_ < NREAD; ++i_) {                   \
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0); /* one MFMA */     \
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0); /* one LDS read */ \
-    }                                                                        \
-    __builtin_amdgcn_sched_group_barrier(0x008, NMMA - NREAD, 0);            \
-    __builtin_amdgcn_sched_barrier(0);                                       \
-  } while (0)
-    for (int kt = 0; kt < nk; ++kt) {
-#pragma unroll
-      for (int cc = 0; cc < CPS; cc += 2) {
-        const int c = kt * CPS + cc;
-        AFLEX_GEMM_READ(fa1, fb1, c + 1);
-        AFLEX_GEMM_MMA(fa0, fb0);
-        AFLEX_GEMM_INTERLEAVE();
-        if (cc + 2 == CPS) {
-          AFLEX_GEMM_STAGE(kt + 1);
-          __builtin_amdgcn_sched_barrier(0);
-        }
-        AFLEX_GEMM_READ(fa0, fb0, min(c + 2, nchunks - 1));
-        AFLEX_GEMM_MMA(fa1, fb1);
-        AFLEX_GEMM_INTERLEAVE();
-      }
-    }
-#undef AFLEX_GEMM_INTERLEAVE
-    // no load may still target LDS when the work-group retires
+    for (int kt = 0; kt < nk; ++kt) AFLEX_GEMM_STAGE(kt + 1);
     __builtin_amdgcn_s_waitcnt(0);
+  } else if (nk > 0) {
+    auto kloop = [&](auto tma) {
+      constexpr int TMA = decltype(tma)::value;
+      bf16x8 fa0[TMA], fb0[NB][TN], fa1[TMA], fb1[NB][TN];
+#pragma unroll
+      for (int st = 0; st < STAGES - 1; ++st) AFLEX_GEMM_ISSUE(sm[st], st);
+      AFLEX_GEMM_STAGE(0);
+      AFLEX_GEMM_READ(fa0, fb0, 0, TMA);
+      static_assert(CPS % 2 == 0, "an even number of MFMA k-chunks per stage");
+      // One MFMA, one fragment read, alternately, then whichever kind remains.
+      constexpr int NREAD = TMA + NB * TN, NMMA = NB * TMA * TN;
+      constexpr int NPAIR = NREAD < NMMA ? NREAD : NMMA;
+#define AFLEX_GEMM_INTERLEAVE()                                                              \
+  do {                                                                                       \
+    _Pragma("unroll") for (int i_ = 0; i_ < NPAIR; ++i_) {                                   \
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0); /* one MFMA */                     \
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0); /* one LDS read */                 \
+    }                                                                                        \
+    if constexpr (NMMA > NREAD) __builtin_amdgcn_sched_group_barrier(0x008, NMMA - NREAD, 0); \
+    if constexpr (NREAD > NMMA) __builtin_amdgcn_sched_group_barrier(0x100, NREAD - NMMA, 0); \
+    __builtin_amdgcn_sched_barrier(0);                                                       \
+  } while (0)
+      for (int kt = 0; kt < nk; ++kt) {
+#pragma unroll
+        for (int cc = 0; cc < CPS; cc += 2) {
+          const int c = kt * CPS + cc;
+          AFLEX_GEMM_READ(fa1, fb1, c + 1, TMA);
+          AFLEX_GEMM_MMA(fa0, fb0, TMA);
+          AFLEX_GEMM_INTERLEAVE();
+          if (cc + 2 == CPS) {
+            AFLEX_GEMM_STAGE(kt + 1);
+            __builtin_amdgcn_sched_barrier(0);
+          }
+          AFLEX_GEMM_READ(fa0, fb0, min(c + 2, nchunks - 1), TMA);
+          AFLEX_GEMM_MMA(fa1, fb1, TMA);
+          AFLEX_GEMM_INTERLEAVE();
+        }
+      }
+#undef AFLEX_GEMM_INTERLEAVE
+      // no load may still target LDS when the work-group retires
+      __builtin_amdgcn_s_waitcnt(0);
+    };
+    using I1 = std::integral_constant<int, 1>;
+    using I2 = std::integral_constant<int, 2 <= TM ? 2 : TM>;
+    using I3 = std::integral_constant<int, 3 <= TM ? 3 : TM>;
+    using IT = std::integral_constant<int, TM>;
+    static_assert(TM <= 4, "row blocks per wave");
+    if (nact == 1)
+      kloop(I1{});
+    else if (nact == 2)
+      kloop(I2{});
+    else if (nact == 3)
+      kloop(I3{});
+    else
+      kloop(IT{});
   }
 #undef AFLEX_GEMM_READ
 #undef AFLEX_GEMM_MMA
