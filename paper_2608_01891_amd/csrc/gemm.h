@@ -265,16 +265,6 @@ __global__ __launch_bounds__(64 * WM * WN, LDS_BYTES > 81920 ? 1 : 2) void gemm_
     AFLEX_GEMM_ISSUE(sm[((KT1) + STAGES - 1) % STAGES], (KT1) + STAGES - 1);              \
   } while (0)
 
-  // Software pipeline over k-chunks (an even number per stage):
-  // the fragment reads of chunk c+1 are interleaved one by one with the MFMAs
-  // of chunk c (the wave issues in order, so a read placed between two MFMAs
-  // goes out while the first executes); the stage wait and barrier follow,
-  // then the reads of chunk c+2 interleaved with the MFMAs of chunk c+1. The
-  // body has no data-dependent guards, so the only LDS waits are for reads
-  // issued a chunk earlier; the last iteration's stage step and read of
-  // chunk c+2 re-read the last k-step (clamped), which is never used.
-  // Measured against the guarded two-chunk loop (whose waits covered the
-  // reads just issued): 4-5% at the MFMA-bound shapes, bit-identical.
   // Row blocks of this wave that hold rows of the tile: a partly filled row
   // tile (an expert's last rows, a dense remainder) multiplies only those.
   const int nact = (min(max(row1 - row0 - wm * WTM, 0), WTM) + MS - 1) / MS;
@@ -288,6 +278,16 @@ __global__ __launch_bounds__(64 * WM * WN, LDS_BYTES > 81920 ? 1 : 2) void gemm_
     for (int kt = 0; kt < nk; ++kt) AFLEX_GEMM_STAGE(kt + 1);
     __builtin_amdgcn_s_waitcnt(0);
   } else if (nk > 0) {
+    // Software pipeline over k-chunks (an even number per stage):
+    // the fragment reads of chunk c+1 are interleaved one by one with the MFMAs
+    // of chunk c (the wave issues in order, so a read placed between two MFMAs
+    // goes out while the first executes); the stage wait and barrier follow,
+    // then the reads of chunk c+2 interleaved with the MFMAs of chunk c+1. The
+    // body has no data-dependent guards, so the only LDS waits are for reads
+    // issued a chunk earlier; the last iteration's stage step and read of
+    // chunk c+2 re-read the last k-step (clamped), which is never used.
+    // Measured against the guarded two-chunk loop (whose waits covered the
+    // reads just issued): 4-5% at the MFMA-bound shapes, bit-identical.
     auto kloop = [&](auto tma) {
       constexpr int TMA = decltype(tma)::value;
       bf16x8 fa0[TMA], fb0[NB][TN], fa1[TMA], fb1[NB][TN];
