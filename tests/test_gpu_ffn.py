@@ -55,10 +55,12 @@ def test_qwen3_prefill_tokens_sampled(gpu_lib, qwen3_weights):
     check_rows(y[rows], ref, what="qwen3 swiglu prefill T=4096 (sampled)")
 
 
-@pytest.mark.parametrize("T", [32, 33, 64, 65, 255, 257])
+@pytest.mark.parametrize("T", [32, 33, 64, 65, 100, 255, 257, 300, 406, 456, 511])
 def test_tile_plan_boundaries(gpu_lib, T):
-    """Token counts on both sides of the dense tile-size thresholds and a
-    256-row tile with a one-row tail."""
+    """Token counts on both sides of the dense tile-size thresholds, and
+    partly filled last row tiles whose waves multiply 0 to 4 of their row
+    blocks (128-row tile with 100 rows; 256-row tails of 1, 44, 150, 200 and
+    255 rows)."""
     x, w, _ = synth.custom_ffn(120 + T, T, 320, 640)
     y = aflex.ffn_swiglu(x.to(DEV), w.to(DEV)).cpu()
     check_rows(y, oracle.swiglu_ffn(x, w.w_gate, w.w_up, w.w_down), what=f"swiglu T={T}")
