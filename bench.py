@@ -601,8 +601,13 @@ def main():
             ms, kk = timed_kernels(lambda: aflex.attn_prefill(pw, out=outp), 10, ["attn_prefill"], aflex)
             pflops = sum(4.0 * n * (n + 1) / 2 * pw.Hq * pw.D for n in pw.lens)
             tag = f"prefill_attention_{model.split('-')[0]}_{nprompt}x{plen}"
+            # bytes the kernel must move: q in and out once, K and V of each KV head once
+            pbytes = 2 * pw.T * pw.Hq * pw.D * 2 + 2 * pw.T * pw.Hkv * pw.D * 2
+            patt = min(PEAK_BF16, pflops / pbytes * PEAK_HBM)
             ops[tag] = {"ms": round(ms, 5), "tflops": round(pflops / (ms * 1e-3) / 1e12, 1),
                         "mfma_frac": round(pflops / (ms * 1e-3) / PEAK_BF16, 4),
+                        "GB_per_s": round(pbytes / (ms * 1e-3) / 1e9, 1),
+                        "attainable_frac": round(pflops / (ms * 1e-3) / patt, 4),
                         "tok_per_s": round(pw.T / (ms * 1e-3), 1),
                         "kernels": kk}
             if plen == 4096 and model == "qwen3-32b":
