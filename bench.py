@@ -92,7 +92,9 @@ def timed_kernels(fn, reps, names, aflex):
 
 
 def energy_reader():
-    """Callable returning the GPU's accumulated energy in joules, or None."""
+    """Callable returning (accumulated energy in J, the counter's own timestamp
+    in s) for the GPU, or None. The counter advances in bursts, so energy is
+    divided by the counter's timestamps, not by the host's clock."""
     try:
         import amdsmi
         amdsmi.amdsmi_init()
@@ -101,11 +103,40 @@ def energy_reader():
         def read():
             e = amdsmi.amdsmi_get_energy_count(h)
             acc = e.get("energy_accumulator", e.get("power"))
-            return float(acc) * float(e["counter_resolution"]) * 1e-6
+            return float(acc) * float(e["counter_resolution"]) * 1e-6, float(e["timestamp"]) * 1e-9
         read()
         return read
     except Exception:
         return None
+
+
+def steady_power(fn, read_energy, secs=4.0):
+    """Average board power (W) while fn() is issued back to back: the energy
+    counter is read twice inside the busy period, 1 s after its start and 1 s
+    before its end, and the energy between the two readings is divided by the
+    time between the counter's own timestamps. The host keeps at most ~40
+    calls queued."""
+    import torch
+    ev, s0, s1, n = [], None, None, 0
+    t0 = time.perf_counter()
+    while True:
+        fn()
+        n += 1
+        if n % 20 == 0:
+            e = torch.cuda.Event()
+            e.record()
+            ev.append(e)
+            if len(ev) > 2:
+                ev.pop(0).synchronize()
+        el = time.perf_counter() - t0
+        if s0 is None and el >= 1.0:
+            s0 = read_energy()
+        if s1 is None and el >= secs - 1.0:
+            s1 = read_energy()
+        if el >= secs:
+            break
+    torch.cuda.synchronize()
+    return (s1[0] - s0[0]) / (s1[1] - s0[1]) if s1[1] > s0[1] else float("nan")
 
 
 def clock_reader():
@@ -350,20 +381,20 @@ def main():
     read_energy = energy_reader()
     read_clock = clock_reader()
     if read_energy is not None:
-        n = max(1, int(1.5 / (ms_step * 1e-3)))
-        torch.cuda.synchronize()
-        e0, t0 = read_energy(), time.perf_counter()
-        for _ in range(n):
-            step()
+        watts = steady_power(step, read_energy)
         clocks = []
-        if read_clock is not None:  # sampled while the queued steps run
+        if read_clock is not None:  # sampled while queued steps run
+            for _ in range(8):
+                step()
             for _ in range(10):
-                time.sleep(0.05)
+                time.sleep(0.002)
                 clocks.append(read_clock())
-        torch.cuda.synchronize()
-        e1, t1 = read_energy(), time.perf_counter()
-        result["energy"] = {"joules_per_token": round((e1 - e0) / (n * B), 6),
-                            "avg_watts": round((e1 - e0) / (t1 - t0), 1), "steps": n}
+            torch.cuda.synchronize()
+        result["energy"] = {"joules_per_token": round(watts * ms_step * 1e-3 / B, 6),
+                            "avg_watts": round(watts, 1),
+                            "method": "board power in steady state (energy counter and its timestamps "
+                                      "read twice inside 4 s of back-to-back steps) x measured step "
+                                      "time / tokens"}
         if clocks:
             result["energy"]["gfx_clock_mhz"] = {"min": min(clocks), "max": max(clocks),
                                                  "mean": round(sum(clocks) / len(clocks), 1)}
@@ -404,6 +435,17 @@ def main():
             off += n
         variants["standalone_sum_ms"] = {"attention": round(t_a, 4), "ffn": round(t_f, 4),
                                          "serial": round(t_a + t_f, 4)}
+        # energy per token of each operator alone (the last microbatch, back to
+        # back for about a second each): the single-GPU view of DA against DF
+        if read_energy is not None:
+            def energy_of(fn, tokens):
+                ms_each = timed(fn, 10)
+                watts = steady_power(fn, read_energy)
+                return {"J_per_token": round(watts * ms_each * 1e-3 / tokens, 6),
+                        "avg_watts": round(watts, 1), "ms_per_call": round(ms_each, 4)}
+            variants["energy_per_operator"] = {
+                "attention_microbatch": energy_of(lambda: aflex.attn_decode(am, out=out), n),
+                "moe_ffn_microbatch": energy_of(lambda: aflex.moe_ffn(xm, f, lm, k, y=x_mb[:n]), n)}
         variants["eq2_ms"] = {"M=1": round(plan.eq2_layer_time(t_a, t_f, 0.0, 1), 4),
                               "M=4": round(plan.eq2_layer_time(t_a, t_f, 0.0, 4), 4)}
         variants["byte_roofline_ms"] = round(step_bytes / PEAK_HBM * 1e3, 4)
