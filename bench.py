@@ -139,6 +139,14 @@ def steady_power(fn, read_energy, secs=4.0):
     return (s1[0] - s0[0]) / (s1[1] - s0[1]) if s1[1] > s0[1] else float("nan")
 
 
+def energy_of(fn, tokens, read_energy):
+    """J/token and board power of fn() run back to back (tokens per call)."""
+    ms_each = timed(fn, 10)
+    watts = steady_power(fn, read_energy)
+    return {"J_per_token": round(watts * ms_each * 1e-3 / tokens, 6),
+            "avg_watts": round(watts, 1), "ms_per_call": round(ms_each, 4)}
+
+
 def clock_reader():
     """Callable returning the current graphics clock in MHz, or None."""
     try:
@@ -438,14 +446,9 @@ def main():
         # energy per token of each operator alone (the last microbatch, back to
         # back for about a second each): the single-GPU view of DA against DF
         if read_energy is not None:
-            def energy_of(fn, tokens):
-                ms_each = timed(fn, 10)
-                watts = steady_power(fn, read_energy)
-                return {"J_per_token": round(watts * ms_each * 1e-3 / tokens, 6),
-                        "avg_watts": round(watts, 1), "ms_per_call": round(ms_each, 4)}
             variants["energy_per_operator"] = {
-                "attention_microbatch": energy_of(lambda: aflex.attn_decode(am, out=out), n),
-                "moe_ffn_microbatch": energy_of(lambda: aflex.moe_ffn(xm, f, lm, k, y=x_mb[:n]), n)}
+                "attention_microbatch": energy_of(lambda: aflex.attn_decode(am, out=out), n, read_energy),
+                "moe_ffn_microbatch": energy_of(lambda: aflex.moe_ffn(xm, f, lm, k, y=x_mb[:n]), n, read_energy)}
         variants["eq2_ms"] = {"M=1": round(plan.eq2_layer_time(t_a, t_f, 0.0, 1), 4),
                               "M=4": round(plan.eq2_layer_time(t_a, t_f, 0.0, 4), 4)}
         variants["byte_roofline_ms"] = round(step_bytes / PEAK_HBM * 1e3, 4)
@@ -718,6 +721,12 @@ def main():
             sens[name] = row
         torch.cuda.synchronize()
         ops["cu_sensitivity"] = sens
+        if read_energy is not None:  # the same operators on the whole GPU: energy per token
+            toks = {"decode_attention_qwen3_B64": wq.B, "decode_swiglu_qwen3_T32": 32,
+                    "decode_swiglu_qwen3_T512": 512, "prefill_attention_qwen3_2x4096": pw.T}
+            st = torch.cuda.current_stream()
+            ops["energy_per_operator"] = {name: energy_of(lambda fn=fn: fn(st), toks[name], read_energy)
+                                          for name, fn in cases.items()}
         del wd, wq, oq, x32, x512, y32, y512, pw, op_
         result["operators"] = ops
 
