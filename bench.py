@@ -147,6 +147,18 @@ def energy_of(fn, tokens, read_energy):
             "avg_watts": round(watts, 1), "ms_per_call": round(ms_each, 4)}
 
 
+def cpu_model():
+    """The host CPU's model name (/proc/cpuinfo), or None."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
 def clock_reader():
     """Callable returning the current graphics clock in MHz, or None."""
     try:
@@ -801,7 +813,7 @@ def main():
                                           "tok_s": round(256 / (t1 - t0), 2)}
         del mc
         result["cpu_baseline"] = {
-            "value": round(n_seq / dt, 4), "unit": "tok/s", "cores": nthreads,
+            "value": round(n_seq / dt, 4), "unit": "tok/s", "cores": nthreads, "cpu_model": cpu_model(),
             "kind": "oracle",
             "sample": f"first {n_seq} of the 256 sequences of the pipeline workload ({ntok} cached "
                       f"tokens): their attention and top-2 MoE FFN in the float64 oracle, {dt:.1f} s",
