@@ -8,11 +8,15 @@
 //
 // Work decomposition: one work-group per (query head, prompt, 128-row query
 // tile); its 4 waves own 32 query rows each and walk the prompt's keys in
-// tiles of 64 up to the causal limit of their rows. Query tiles are dispatched
+// tiles of 64 up to the causal limit of their rows. For batches with prompts
+// of 2048 tokens or more and an even number of query heads per KV head, a
+// work-group of 8 waves takes two heads of one KV group, so each staged K/V
+// tile serves both (one such work-group per CU; shorter prompts run faster
+// with two 4-wave work-groups per CU). Query tiles are dispatched
 // longest-first (they are the slow index of the grid, reversed) so the short
-// diagonal tiles fill the tail. When Hq is a multiple of 8 the head index is
-// permuted so that the heads sharing one KV head run on the same XCD and
-// share its L2.
+// diagonal tiles fill the tail. When the number of head blocks is a multiple
+// of 8 it is permuted so that the heads sharing one KV head run on the same
+// XCD and share its L2.
 //
 // K and V tiles (64 keys x 128 d, row-major, 16-byte chunks XOR-swizzled by
 // row so that both kinds of fragment read are free of bank conflicts) stream from HBM straight into double-buffered LDS (direct global->LDS
@@ -48,6 +52,10 @@ constexpr int kPM = 128;  // query rows per work-group
 constexpr int kPN = 64;   // keys per tile
 constexpr int kPD = 128;  // head dimension
 constexpr int kTile = kPN * kPD * 2;  // bytes of one K or V tile
+// Prompts at least this long run two query heads of a KV group per
+// work-group (8 waves sharing each staged K/V tile, one work-group per CU);
+// shorter ones one head (4 waves, two work-groups per CU).
+constexpr int kTwoHeadMinLen = 2048;
 
 struct PrefillParams {
   const uint16_t* q;
@@ -86,11 +94,13 @@ __device__ __forceinline__ float max_across_halves(float x) {
   return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
 }
 
-__global__ __launch_bounds__(256, 2) void attn_prefill_kernel(PrefillParams p) {
+template <int HPW>
+__global__ __launch_bounds__(256 * HPW, HPW == 1 ? 2 : 1) void attn_prefill_kernel(PrefillParams p) {
   __shared__ __attribute__((aligned(16))) uint8_t smem[4 * kTile];  // K0, K1, V0, V1
 
-  int h = blockIdx.x;
-  if ((p.Hq & 7) == 0) h = (h & 7) * (p.Hq >> 3) + (h >> 3);
+  const int nhb = p.Hq / HPW;
+  int hb = blockIdx.x;
+  if ((nhb & 7) == 0) hb = (hb & 7) * (nhb >> 3) + (hb >> 3);
   const int b = blockIdx.y;
   const int tile = p.ntiles - 1 - (int)blockIdx.z;
   int s1 = p.cu[b + 1], s0 = p.cu[b];
@@ -100,9 +110,10 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_kernel(PrefillParams p) {
   const int q0 = tile * kPM;
   if (q0 >= n) return;
 
-  const int g = h / p.G;
   const int tid = threadIdx.x, w = tid >> 6, l = tid & 63, lr = l & 31, hi = l >> 5;
-  const int qr0 = q0 + w * 32;     // first query row of this wave
+  const int h = hb * HPW + (w >> 2);  // query head of this wave
+  const int g = h / p.G;
+  const int qr0 = q0 + (w & 3) * 32;  // first query row of this wave
   const int qi = qr0 + lr;         // this lane's query row (a column of S^T)
   const size_t qstride = (size_t)p.Hq * kPD, kvstride = (size_t)p.Hkv * kPD;
 
@@ -120,21 +131,22 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_kernel(PrefillParams p) {
   const uint16_t* vbase = p.v + (size_t)s0 * kvstride + (size_t)g * kPD;
   const uint32_t lds0 = lds_offset(smem);
 
-  // Staging: wave-load i of thread tid fills slot i * 256 + tid of the tile,
-  // i.e. row i * 16 + tid / 16 and stored chunk tid % 16; the logical chunk is
-  // the same for all four wave-loads of a thread.
+  // Staging: wave-load i of thread tid fills slot i * 256 HPW + tid of the
+  // tile, i.e. row i * 16 HPW + tid / 16 and stored chunk tid % 16; the logical
+  // chunk is the same for all 4 / HPW wave-loads of a thread.
   const int srow = tid >> 4, schunk = (tid & 15) ^ kv_swz(srow);
+  constexpr int RPL = 16 * HPW;  // tile rows per wave-load round of the work-group
   const size_t soff = (size_t)srow * kvstride + schunk * 8;
   auto issue = [&](const uint16_t* base, int kt, uint32_t lds) {
     lds += w * 1024;
     if (kt * kPN + kPN <= n) {
 #pragma unroll
-      for (int i = 0; i < 4; ++i) lds_dma16(base + soff + (size_t)(kt * kPN + i * 16) * kvstride, lds + i * 4096);
+      for (int i = 0; i < 4 / HPW; ++i) lds_dma16(base + soff + (size_t)(kt * kPN + i * RPL) * kvstride, lds + i * 4096 * HPW);
     } else {  // tail tile: rows past the prompt re-read its last row (masked / weighted 0)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int key = min(kt * kPN + i * 16 + srow, n - 1);
-        lds_dma16(base + (size_t)key * kvstride + schunk * 8, lds + i * 4096);
+      for (int i = 0; i < 4 / HPW; ++i) {
+        const int key = min(kt * kPN + i * RPL + srow, n - 1);
+        lds_dma16(base + (size_t)key * kvstride + schunk * 8, lds + i * 4096 * HPW);
       }
     }
   };
@@ -314,7 +326,10 @@ hipError_t launch_attn_prefill(const aflex_prefill_args& a, hipStream_t stream) 
   const float scale = a.scale > 0.f ? a.scale : 1.f / sqrtf((float)a.D);
   p.c = scale * kLog2e;
   ProfScope ps("attn_prefill", stream);
-  attn_prefill_kernel<<<dim3(a.Hq, a.B, p.ntiles), 256, 0, stream>>>(p);
+  if (p.G % 2 == 0 && a.max_seqlen >= kTwoHeadMinLen)
+    attn_prefill_kernel<2><<<dim3(a.Hq / 2, a.B, p.ntiles), 512, 0, stream>>>(p);
+  else
+    attn_prefill_kernel<1><<<dim3(a.Hq, a.B, p.ntiles), 256, 0, stream>>>(p);
   return hipGetLastError();
 }
 

@@ -126,6 +126,26 @@ def test_long_prompt_sampled(gpu_lib):
     check_rows(out[rows], ref[rows], what="prefill n=16384 (sampled)")
 
 
+@pytest.mark.parametrize("Hq,Hkv", [(8, 2), (12, 6), (64, 8)])
+def test_two_heads_per_work_group_sampled(gpu_lib, Hq, Hkv):
+    """Batches with a prompt of at least 2048 tokens and an even number of
+    query heads per KV head run two heads per work-group: ragged long
+    prompts beside a short and an empty one, sampled rows of every prompt
+    (first, last, the diagonal tiles' edges); Hq / 2 not a multiple of 8 in the
+    second case."""
+    lens = [2048, 2100, 0, 5, 2300]
+    p = synth.make_prefill(57 + Hq, lens, Hq, Hkv, 128, device=DEV)
+    out = aflex.attn_prefill(p).cpu()
+    pc = p.to("cpu")
+    cu = [int(c) for c in pc.cu_seqlens]
+    rows = []
+    for b, n in enumerate(lens):
+        if n:
+            rows += sorted({cu[b] + r for r in (0, min(63, n - 1), min(127, n - 1), min(128, n - 1), n // 2, n - 2, n - 1) if 0 <= r < n})
+    ref = oracle.attention_prefill(pc.q, pc.k, pc.v, pc.cu_seqlens, rows=rows)
+    check_rows(out[rows], ref[rows], what=f"prefill two heads per work-group Hq={Hq} Hkv={Hkv} (sampled)")
+
+
 def test_kv_write_long_prompt_bit_exact(gpu_lib):
     n = 5000
     a = synth.custom_attention(56, 1, 8, 8, 128, [n], ctx_hi=n)
