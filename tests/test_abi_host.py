@@ -21,10 +21,18 @@ def lib():
 
 def test_exports_every_declared_symbol(lib):
     names = aflex.exported_names()
-    assert len(names) == 21
+    assert len(names) == 22
     for n in names:
         assert hasattr(lib, n), n
     assert lib.aflex_version().startswith(b"aflex")
+
+
+def test_teardown_with_nothing_cached(lib):
+    """The teardown call destroys only what the library created; with nothing
+    created yet it succeeds without touching a device, and it may repeat."""
+    assert lib.aflex_teardown() == aflex.OK
+    assert lib.aflex_teardown() == aflex.OK
+    aflex.close()
 
 
 def _attn(**kw):

@@ -5,7 +5,6 @@ import torch
 
 import oracle
 from paper_2608_01891_amd import aflex, synth
-from tests.helpers import sample_rows, sub_attention
 from tests.parity import check_rows
 
 pytestmark = pytest.mark.gpu
@@ -42,24 +41,22 @@ def test_full_1024_token_splits(gpu_lib, split):
     check_rows(out, _oracle(a), what=f"1024-token splits (split={split})")
 
 
-def test_qwen3_shape_sampled(gpu_lib):
+def test_qwen3_shape_all_rows(gpu_lib):
+    """The Qwen3-32B workload at full size (B = 64, 64/8 heads, lognormal
+    contexts): every sequence and head against the oracle."""
     w = synth.qwen3_attention(device=DEV)
     a = w.attn
     out = aflex.attn_decode(a).cpu()
-    ctx = a.context_lens.cpu()
-    rows = sample_rows(a.B, 10, seed=1, must=[int(ctx.argmax()), int(ctx.argmin())])
-    sub = sub_attention(a, rows)
-    check_rows(out[rows], _oracle(sub), what="qwen3 attention (sampled)")
-    assert torch.isfinite(out.float()).all()
+    check_rows(out, _oracle(a.to("cpu")), what="qwen3 attention (all 64 sequences)")
 
 
-def test_long_context_shape_sampled(gpu_lib):
+def test_long_context_shape_all_rows(gpu_lib):
+    """The pipeline workload's attention at full size (B = 256, 32/8 heads,
+    contexts up to 22384 tokens, 1024-token splits): every row."""
     w = synth.af_pipeline(device=DEV)
     a = w.attn
     out = aflex.attn_decode(a).cpu()
-    ctx = a.context_lens.cpu()
-    rows = sample_rows(a.B, 6, seed=2, must=[int(ctx.argmax()), int(ctx.argmin())])
-    check_rows(out[rows], _oracle(sub_attention(a, rows)), what="long-context attention (sampled)")
+    check_rows(out, _oracle(a.to("cpu")), what="long-context attention (all 256 sequences)")
 
 
 def test_context_one_is_v_bitwise(gpu_lib):

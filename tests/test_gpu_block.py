@@ -4,7 +4,6 @@ import torch
 
 import oracle
 from paper_2608_01891_amd import aflex, synth
-from tests.helpers import sample_rows
 from tests.parity import check_rows
 
 pytestmark = pytest.mark.gpu
@@ -62,9 +61,10 @@ def test_linear_shapes(gpu_lib, T, K, N):
 
 
 @pytest.mark.parametrize("T,K,N", [(64, 8192, 5120), (256, 4096, 4096)])
-def test_output_projection_shapes_sampled(gpu_lib, T, K, N):
+def test_output_projection_shapes_all_rows(gpu_lib, T, K, N):
+    """o_proj at the Qwen3-32B (64 x 8192 -> 5120) and Mixtral (256 x 4096 ->
+    4096) decode shapes: every row."""
     x = synth.normal_tensor(99, 4, (T, K), device=DEV)
     w = synth.normal_tensor(99, 8, (N, K), scale=0.02, device=DEV)
     y = aflex.linear(x, w).cpu()
-    rows = sample_rows(T, 8, seed=T, must=[0, T - 1])
-    check_rows(y[rows], oracle.linear(x[rows].cpu(), w.cpu()), what=f"o_proj T={T}")
+    check_rows(y, oracle.linear(x.cpu(), w.cpu()), what=f"o_proj T={T}")

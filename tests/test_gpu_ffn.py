@@ -33,26 +33,29 @@ def qwen3_weights():
 
 
 @pytest.mark.parametrize("T", [32, 128, 256, 512])
-def test_qwen3_shape_sampled(gpu_lib, qwen3_weights, T):
+def test_qwen3_shape_all_rows(gpu_lib, qwen3_weights, T):
+    """Qwen3-32B SwiGLU at every decode batch of the workload, every row."""
     w, (wg, wu, wd) = qwen3_weights
     wl = synth.qwen3_swiglu(T, device=DEV, weights=w)
     y = aflex.ffn_swiglu(wl.x, w).cpu()
-    rows = sample_rows(T, 6, seed=T, must=[0, T - 1])
-    ref = oracle.swiglu_ffn(wl.x[rows].cpu(), wg, wu, wd)
-    check_rows(y[rows], ref, what=f"qwen3 swiglu T={T} (sampled)")
+    ref = oracle.swiglu_ffn(wl.x.cpu(), wg, wu, wd)
+    check_rows(y, ref, what=f"qwen3 swiglu T={T} (all rows)")
     y2 = aflex.ffn_swiglu(wl.x, w).cpu()
     assert torch.equal(y, y2)
 
 
-def test_qwen3_prefill_tokens_sampled(gpu_lib, qwen3_weights):
-    """The dense FFN over a prefill batch: two 2048-token prompts at once (T = 4096)."""
+def test_qwen3_prefill_tokens_every_row_tile(gpu_lib, qwen3_weights):
+    """The dense FFN over a prefill batch: two 2048-token prompts at once
+    (T = 4096), the first and last row of every 256-row block plus random
+    rows."""
     w, (wg, wu, wd) = qwen3_weights
     T = 4096
     x = synth.prefill_ffn_tokens(5120, T, device=DEV)
     y = aflex.ffn_swiglu(x, w).cpu()
-    rows = sample_rows(T, 6, seed=T, must=[0, 255, 256, T - 1])
+    edges = [r for t0 in range(0, T, 256) for r in (t0, t0 + 255)]
+    rows = sample_rows(T, len(edges) + 8, seed=T, must=edges)
     ref = oracle.swiglu_ffn(x[rows].cpu(), wg, wu, wd)
-    check_rows(y[rows], ref, what="qwen3 swiglu prefill T=4096 (sampled)")
+    check_rows(y[rows], ref, what="qwen3 swiglu prefill T=4096 (every 256-row block)")
 
 
 @pytest.mark.parametrize("T", [32, 33, 64, 65, 100, 255, 257, 300, 406, 456, 511])

@@ -62,47 +62,63 @@ def mixtral():
     del wl
 
 
-def test_mixtral_shape(gpu_lib, mixtral):
+def _tokens_of_every_pair_block(logits, k, E, block=256):
+    """Tokens of the first and last (token, slot) pair of every block of
+    ``block`` consecutive pairs in each expert's segment of the pair order:
+    rows that cover every row tile of the grouped GEMMs."""
+    ids, _ = oracle.route_topk(logits.cpu(), k)
+    _, offsets, sorted_ids, _ = oracle.routing_tables(ids, E)
+    toks = set()
+    for e in range(E):
+        lo, hi = int(offsets[e]), int(offsets[e + 1])
+        for p0 in range(lo, hi, block):
+            for p in (p0, min(p0 + block, hi) - 1):
+                toks.add(int(sorted_ids[p]) // k)
+    return sorted(toks)
+
+
+def test_mixtral_shape_all_rows(gpu_lib, mixtral):
     wl = mixtral
     y, r = aflex.moe_ffn(wl.x, wl.ffn, wl.router_logits, 2, routing=True)
     ids = _check_routing(r, wl.router_logits, 2, 8)
     counts = torch.bincount(ids.reshape(-1), minlength=8)
     assert counts.tolist() == [62, 61, 76, 65, 63, 67, 56, 62]
     y = y.cpu()
-    toks = sample_rows(256, 6, seed=3, must=[0, 255])
     f = wl.ffn
     ref, _, _ = oracle.moe_ffn(wl.x.cpu(), wl.router_logits.cpu(), f.w_gate.cpu(), f.w_up.cpu(),
-                               f.w_down.cpu(), 2, token_indices=toks)
-    check_rows(y[toks], ref[toks], what="mixtral moe (sampled)")
+                               f.w_down.cpu(), 2)
+    check_rows(y, ref, what="mixtral moe T=256 (all rows)")
     y2 = aflex.moe_ffn(wl.x, wl.ffn, wl.router_logits, 2).cpu()
     assert torch.equal(y, y2)
 
 
-def test_mixtral_2048_tokens_sampled(gpu_lib, mixtral):
+def test_mixtral_2048_tokens_all_rows(gpu_lib, mixtral):
     """The MoE at 2048 tokens (seed 103), the MFMA-bound decode size timed by the
-    benchmark: 256-row tiles, routing in three kernels."""
+    benchmark (256-row tiles, routing in three kernels): every row."""
     T = 2048
     wl = synth.mixtral_moe(device=DEV, T=T, seed=103, weights=mixtral.ffn)
     y, r = aflex.moe_ffn(wl.x, wl.ffn, wl.router_logits, 2, routing=True)
     _check_routing(r, wl.router_logits, 2, 8)
-    toks = sample_rows(T, 6, seed=103, must=[0, T - 1])
     f = wl.ffn
     ref, _, _ = oracle.moe_ffn(wl.x.cpu(), wl.router_logits.cpu(), f.w_gate.cpu(), f.w_up.cpu(),
-                               f.w_down.cpu(), 2, token_indices=toks)
-    check_rows(y.cpu()[toks], ref[toks], what="mixtral moe T=2048 (sampled)")
+                               f.w_down.cpu(), 2)
+    check_rows(y.cpu(), ref, what="mixtral moe T=2048 (all rows)")
 
 
-def test_mixtral_prefill_tokens_sampled(gpu_lib, mixtral):
-    """The MoE FFN over a prefill batch (T = 4096 tokens, 8192 token/slot pairs)."""
+def test_mixtral_prefill_tokens_every_row_tile(gpu_lib, mixtral):
+    """The MoE FFN over a prefill batch (T = 4096 tokens, 8192 token/slot
+    pairs): the tokens of the first and last pair of every 256-pair block of
+    each expert, plus random tokens."""
     T = 4096
     wl = synth.mixtral_moe(device=DEV, T=T, seed=7, weights=mixtral.ffn)
     y, r = aflex.moe_ffn(wl.x, wl.ffn, wl.router_logits, 2, routing=True)
     _check_routing(r, wl.router_logits, 2, 8)
-    toks = sample_rows(T, 6, seed=7, must=[0, T - 1])
+    edges = _tokens_of_every_pair_block(wl.router_logits, 2, 8)
+    toks = sample_rows(T, len(edges) + 8, seed=7, must=edges + [0, T - 1])
     f = wl.ffn
     ref, _, _ = oracle.moe_ffn(wl.x.cpu(), wl.router_logits.cpu(), f.w_gate.cpu(), f.w_up.cpu(),
                                f.w_down.cpu(), 2, token_indices=toks)
-    check_rows(y.cpu()[toks], ref[toks], what="mixtral moe prefill T=4096 (sampled)")
+    check_rows(y.cpu()[toks], ref[toks], what="mixtral moe prefill T=4096 (every pair block)")
 
 
 @pytest.mark.parametrize("T,E,k", [(200, 64, 8), (33, 64, 1), (64, 2, 2), (512, 8, 2), (513, 8, 2),

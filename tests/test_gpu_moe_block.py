@@ -11,7 +11,6 @@ import torch
 
 import oracle
 from paper_2608_01891_amd import aflex, synth
-from tests.helpers import sample_rows
 from tests.parity import check_rows
 
 pytestmark = pytest.mark.gpu
@@ -56,7 +55,7 @@ def test_small_shapes(gpu_lib, T, H, I, E, k, res):
     _check(y, lg, r, ref_y, ref_lg, ref_ids, k)
 
 
-def test_mixtral_shape_sampled(gpu_lib):
+def test_mixtral_shape_all_rows(gpu_lib):
     T, H, I, E, k = 256, 4096, 14336, 8, 2
     x, _, _ = synth.custom_ffn(130, T, H, 64, E=E)
     w = synth.make_ffn_weights(130, H, I, E, device=DEV)
@@ -64,7 +63,6 @@ def test_mixtral_shape_sampled(gpu_lib):
     wr = synth.normal_tensor(130, 51, (E, H), scale=0.02)
     y, lg, r = aflex.moe_block(x.to(DEV), w, gamma.to(DEV), wr.to(DEV), k, eps=1e-5, residual=True,
                                routing=True)
-    toks = sample_rows(T, 6, seed=5, must=[0, T - 1])
     ref_y, ref_lg, ref_ids = oracle.moe_block(x, gamma, 1e-5, wr, w.w_gate.cpu(), w.w_up.cpu(),
-                                              w.w_down.cpu(), k, True, token_indices=toks)
-    _check(y, lg, r, ref_y, ref_lg, ref_ids, k, rows=toks)
+                                              w.w_down.cpu(), k, True)
+    _check(y, lg, r, ref_y, ref_lg, ref_ids, k)

@@ -4,7 +4,6 @@ import torch
 
 import oracle
 from paper_2608_01891_amd import aflex, synth
-from tests.helpers import sample_rows
 from tests.parity import check_rows
 
 pytestmark = pytest.mark.gpu
@@ -55,16 +54,39 @@ def test_loose_max_seqlen_and_determinism(gpu_lib):
     assert torch.equal(a, b)
 
 
-@pytest.mark.parametrize("model,prompt_len,prompts", [("qwen3-32b", 4096, 2), ("mixtral-8x7b", 128, 32)])
-def test_paper_prompt_lengths_sampled(gpu_lib, model, prompt_len, prompts):
-    p = synth.prefill_workload(model, prompt_len, prompts, device=DEV)
+def _tile_rows(lens, first=True, last=True, tile=128):
+    """Token indices of the first and/or last row of every ``tile``-row query
+    block of every prompt."""
+    rows, start = [], 0
+    for n in lens:
+        for t0 in range(0, n, tile):
+            t1 = min(t0 + tile, n) - 1
+            if first:
+                rows.append(start + t0)
+            if last:
+                rows.append(start + t1)
+        start += n
+    return sorted(set(rows))
+
+
+def test_qwen3_4096_token_prompts_every_query_tile(gpu_lib):
+    """The paper's long input (two 4096-token prompts, Qwen3-32B heads): the
+    first and last row of every 128-row query block of both prompts."""
+    p = synth.prefill_workload("qwen3-32b", 4096, 2, device=DEV)
     out = aflex.attn_prefill(p).cpu()
     pc = p.to("cpu")
-    T = pc.T
-    rows = sample_rows(T, 8, seed=prompt_len,
-                       must=[0, 1, 127, 128, prompt_len - 1, T - 1, T - prompt_len])
+    rows = _tile_rows(pc.lens)
     ref = oracle.attention_prefill(pc.q, pc.k, pc.v, pc.cu_seqlens, rows=rows)
-    check_rows(out[rows], ref[rows], what=f"{model} prefill {prompts}x{prompt_len} (sampled)")
+    check_rows(out[rows], ref[rows], what="qwen3-32b prefill 2x4096 (every query tile)")
+
+
+def test_mixtral_128_token_prompts_all_rows(gpu_lib):
+    """The paper's short input (32 prompts of 128 tokens, Mixtral heads): every row."""
+    p = synth.prefill_workload("mixtral-8x7b", 128, 32, device=DEV)
+    out = aflex.attn_prefill(p).cpu()
+    pc = p.to("cpu")
+    ref = oracle.attention_prefill(pc.q, pc.k, pc.v, pc.cu_seqlens)
+    check_rows(out, ref, what="mixtral-8x7b prefill 32x128 (all rows)")
 
 
 def _cu(new):
@@ -114,16 +136,17 @@ def test_prefill_then_decode_on_the_written_cache(gpu_lib):
     check_rows(out[last], ref[last], what="prefill last rows")
 
 
-def test_long_prompt_sampled(gpu_lib):
+def test_long_prompt_every_query_tile(gpu_lib):
     """One 16384-token prompt at the Qwen3-32B head shape (longer than any of the
-    paper's inputs): sampled rows, including the last."""
+    paper's inputs): one row of every 128-row query block (its first row in
+    even blocks, its last in odd ones), and the prompt's last row."""
     n = 16384
     p = synth.make_prefill(55, [n], 64, 8, 128, device=DEV)
     out = aflex.attn_prefill(p).cpu()
     pc = p.to("cpu")
-    rows = sample_rows(n, 4, seed=5, must=[0, 8191, n - 1])
+    rows = sorted({t0 + (127 if (t0 // 128) % 2 else 0) for t0 in range(0, n, 128)} | {n - 1})
     ref = oracle.attention_prefill(pc.q, pc.k, pc.v, pc.cu_seqlens, rows=rows)
-    check_rows(out[rows], ref[rows], what="prefill n=16384 (sampled)")
+    check_rows(out[rows], ref[rows], what="prefill n=16384 (every query tile)")
 
 
 @pytest.mark.parametrize("Hq,Hkv", [(8, 2), (12, 6), (64, 8)])

@@ -90,3 +90,36 @@ def test_prefill_sweep(gpu_lib, case):
     out = aflex.attn_prefill(p.to(DEV)).cpu()
     ref = oracle.attention_prefill(p.q, p.k, p.v, p.cu_seqlens)
     check_rows(out, ref, what=f"prefill sweep {case}")
+
+
+def _long_prefill_case(rng):
+    """A batch holding one prompt of 2048-2600 tokens (so both prefill kernel
+    shapes are drawn: two query heads per work-group for an even number of
+    heads per KV group, one head otherwise) beside 0-3 prompts of 0-2600."""
+    Hkv = int(rng.integers(1, 3))
+    G = int(rng.choice([1, 2, 3, 4, 8, 16]))
+    lens = [int(n) for n in rng.integers(0, 2601, int(rng.integers(0, 4)))]
+    pos = int(rng.integers(0, len(lens) + 1))
+    lens.insert(pos, int(rng.integers(2048, 2601)))
+    return Hkv * G, Hkv, lens
+
+
+@pytest.mark.parametrize("case", _cases(8, _long_prefill_case, 5))
+def test_long_prefill_sweep(gpu_lib, case):
+    """Rows checked per prompt: first, last, both edges of the first two
+    64-row blocks, the middle and three random rows."""
+    seed, Hq, Hkv, lens = case
+    p = synth.make_prefill(seed, lens, Hq, Hkv, 128, device=DEV)
+    out = aflex.attn_prefill(p).cpu()
+    pc = p.to("cpu")
+    rng = np.random.default_rng(seed)
+    rows, start = set(), 0
+    for n in lens:
+        if n:
+            picks = {0, min(63, n - 1), min(64, n - 1), min(127, n - 1), min(128, n - 1), n // 2, n - 1}
+            picks |= {int(r) for r in rng.integers(0, n, 3)}
+            rows |= {start + r for r in picks}
+        start += n
+    rows = sorted(rows)
+    ref = oracle.attention_prefill(pc.q, pc.k, pc.v, pc.cu_seqlens, rows=rows)
+    check_rows(out[rows], ref[rows], what=f"long prefill sweep {case}")
