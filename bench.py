@@ -91,14 +91,34 @@ def timed_kernels(fn, reps, names, aflex):
     return ms, {kname: round(v[1] / v[0], 5) for kname, v in kp.items()}
 
 
+_SMI = {}
+
+
+def smi_handle():
+    """The first GPU's amdsmi handle, or None. amdsmi is initialised once per
+    process and shut down at interpreter exit."""
+    if "h" not in _SMI:
+        _SMI["h"] = None
+        try:
+            import amdsmi
+            amdsmi.amdsmi_init()
+            import atexit
+            atexit.register(amdsmi.amdsmi_shut_down)
+            _SMI["h"] = amdsmi.amdsmi_get_processor_handles()[0]
+        except Exception:
+            pass
+    return _SMI["h"]
+
+
 def energy_reader():
     """Callable returning (accumulated energy in J, the counter's own timestamp
     in s) for the GPU, or None. The counter advances in bursts, so energy is
     divided by the counter's timestamps, not by the host's clock."""
+    h = smi_handle()
+    if h is None:
+        return None
     try:
         import amdsmi
-        amdsmi.amdsmi_init()
-        h = amdsmi.amdsmi_get_processor_handles()[0]
 
         def read():
             e = amdsmi.amdsmi_get_energy_count(h)
@@ -159,12 +179,32 @@ def cpu_model():
     return None
 
 
+def host_cores():
+    """Logical CPUs this process may run on and the host's physical cores
+    (distinct (socket, core) pairs in /proc/cpuinfo)."""
+    out = {"logical_cpus_available": len(os.sched_getaffinity(0))}
+    try:
+        pairs, phys = set(), None
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("physical id"):
+                    phys = line.split(":", 1)[1].strip()
+                elif line.startswith("core id"):
+                    pairs.add((phys, line.split(":", 1)[1].strip()))
+        if pairs:
+            out["physical_cores_host"] = len(pairs)
+    except OSError:
+        pass
+    return out
+
+
 def clock_reader():
-    """Callable returning the current graphics clock in MHz, or None."""
+    """Callable returning the graphics clock amdsmi reports, in MHz, or None."""
+    h = smi_handle()
+    if h is None:
+        return None
     try:
         import amdsmi
-        amdsmi.amdsmi_init()
-        h = amdsmi.amdsmi_get_processor_handles()[0]
 
         def read():
             c = amdsmi.amdsmi_get_clock_info(h, amdsmi.AmdSmiClkType.GFX)
@@ -352,6 +392,8 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic",
+        "timing": "wall clock over the K timed steps between two device synchronisations, "
+                  "after W untimed warm-up steps; value = 256 tokens x K / that time",
         "config": {"workload": "af-pipeline: Mixtral-8x7B-shaped decode layer step, B=256, "
                                "32/8 heads x 128, paged bf16 KV (block 16, lognormal ctx median 4096, "
                                "sum 1392790 tokens), top-2 of 8 SwiGLU experts H=4096 I=14336, "
@@ -416,8 +458,12 @@ def main():
                                       "read twice inside 4 s of back-to-back steps) x measured step "
                                       "time / tokens"}
         if clocks:
-            result["energy"]["gfx_clock_mhz"] = {"min": min(clocks), "max": max(clocks),
-                                                 "mean": round(sum(clocks) / len(clocks), 1)}
+            # amdsmi reports the clock set for the graphics domain, not the
+            # clock the CUs run at under this load; the counter-derived clock
+            # (GRBM_GUI_ACTIVE cycles over kernel time) is in the profiles.
+            result["energy"]["amdsmi_set_gfx_clock_mhz"] = {
+                "min": min(clocks), "max": max(clocks), "mean": round(sum(clocks) / len(clocks), 1),
+                "note": "set clock as amdsmi reports it; the counters measure 1.7-2.1 GHz under this load"}
     else:
         result["energy"] = "n/a (energy counter not readable)"
 
@@ -505,13 +551,14 @@ def main():
         variants["t_F_over_t_A"] = round(t_f / t_a, 3)
         # A and F pools on one GPU: the two stages' streams on disjoint CU sets
         pools = {}
+        ppws = aflex.Workspace()  # used on the pool streams only, freed before they are released
         for acu in (64, 128, 192):
             pa, pf = aflex.pool_streams(acu, dev)
             for M in (2, 4):
                 m = plan.equal_microbatches(B, M)
 
                 def pstep():
-                    aflex.af_pipeline_step(a, f, logits, k, m, y=y, stream_a=pa, stream_f=pf, ws=pws, join=False)
+                    aflex.af_pipeline_step(a, f, logits, k, m, y=y, stream_a=pa, stream_f=pf, ws=ppws, join=False)
                 pstep()
                 torch.cuda.synchronize()
                 t0 = time.perf_counter()
@@ -521,6 +568,8 @@ def main():
                 pms = (time.perf_counter() - t0) * 1e3 / 5
                 pools[f"attn_cus={acu},M={M}"] = {"ms": round(pms, 4), "tok_per_s": round(B / (pms * 1e-3), 1)}
         variants["cu_pools"] = pools
+        ppws.buf = None
+        aflex.release_pool_streams()
         ops["af_pipeline"] = variants
 
         # Tiny decoder layer (B=4, 8/2 heads x 64, SwiGLU 512 -> 1408): cache-resident,
@@ -732,6 +781,9 @@ def main():
             row["reduction_64_to_256"] = round(1 - row["256_cus_ms"] / row["64_cus_ms"], 3)
             sens[name] = row
         torch.cuda.synchronize()
+        for w_ in wss.values():  # their buffers were used on the pool streams
+            w_.buf = None
+        aflex.release_pool_streams()
         ops["cu_sensitivity"] = sens
         if read_energy is not None:  # the same operators on the whole GPU: energy per token
             toks = {"decode_attention_qwen3_B64": wq.B, "decode_swiglu_qwen3_T32": 32,
@@ -814,6 +866,9 @@ def main():
         del mc
         result["cpu_baseline"] = {
             "value": round(n_seq / dt, 4), "unit": "tok/s", "cores": nthreads, "cpu_model": cpu_model(),
+            "host": host_cores(),
+            "cores_note": "cores = torch CPU threads the oracle ran on; host gives the logical CPUs "
+                          "this process may use and the host's physical cores",
             "kind": "oracle",
             "sample": f"first {n_seq} of the 256 sequences of the pipeline workload ({ntok} cached "
                       f"tokens): their attention and top-2 MoE FFN in the float64 oracle, {dt:.1f} s",

@@ -21,6 +21,7 @@
  *   aflex_attn_prefill      causal attention over packed prompts (prefill)
  *   aflex_pool_streams_*    stream pairs on disjoint CU sets (A/F pools)
  *   aflex_profile_*         per-kernel HIP-event timing
+ *   aflex_teardown          release the HIP events the library caches
  *
  * Conventions shared by every entry point
  *  - bf16 tensors are passed as raw bit patterns (aflex_bf16 = uint16_t).
@@ -292,6 +293,16 @@ aflex_status aflex_pool_streams_destroy(aflex_stream stream_a, aflex_stream stre
 /* ------------------------------------------------------------------------ */
 aflex_status aflex_profile_start(const char *kernels);
 aflex_status aflex_profile_stop(char *report, size_t len);
+
+/* Releases the HIP objects the library keeps between calls: the events that */
+/* order the two streams of aflex_af_pipeline_step (per device) and the       */
+/* timing events of aflex_profile_*. Call it before process exit (or before  */
+/* unloading the library) once no library work is queued on any stream,      */
+/* e.g. after hipDeviceSynchronize(); streams from aflex_pool_streams_create  */
+/* are the caller's to destroy. The library stays usable: the next call      */
+/* creates what it needs again. Errors: HIP if a destroy failed (the others  */
+/* are still destroyed).                                                     */
+aflex_status aflex_teardown(void);
 
 /* Thread-local message describing the last non-OK status of this thread. */
 const char *aflex_last_error(void);

@@ -7,7 +7,9 @@ if the library is not built or no GPU is present, calls raise.
 """
 from __future__ import annotations
 
+import atexit
 import ctypes
+import gc
 import os
 import re
 
@@ -121,10 +123,53 @@ def load():
     lib.aflex_profile_start.restype = ctypes.c_int
     lib.aflex_profile_stop.argtypes = [ctypes.c_char_p, ctypes.c_size_t]
     lib.aflex_profile_stop.restype = ctypes.c_int
+    lib.aflex_teardown.argtypes = []
+    lib.aflex_teardown.restype = ctypes.c_int
     lib.aflex_last_error.restype = ctypes.c_char_p
     lib.aflex_version.restype = ctypes.c_char_p
     _lib = lib
+    atexit.register(close)
     return lib
+
+
+def release_pool_streams():
+    """Destroy the CU-partitioned stream pairs created by pool_streams().
+
+    torch records an event on every stream a tensor was used on (record_stream)
+    when that tensor is freed, so such tensors must go first: this drops the
+    binding's own default workspaces (which record the streams they are used
+    on), waits for the devices and lets torch retire those events, then
+    destroys the streams. Buffers the caller used on the pool streams with
+    record_stream must be freed before the call."""
+    if not _pool_streams:
+        return
+    _default_ws.clear()
+    gc.collect()
+    for d in {key[0] for key in _pool_streams}:
+        torch.cuda.synchronize(d)
+    torch.cuda.empty_cache()
+    first = OK
+    for key in list(_pool_streams):
+        sa, sf = _pool_streams.pop(key)
+        st = _lib.aflex_pool_streams_destroy(_p(sa.cuda_stream), _p(sf.cuda_stream))
+        first = st if first == OK else first
+    _check(first)
+
+
+def close():
+    """Release what the library and this binding hold on the GPU: the pool
+    streams (release_pool_streams) and, once the devices are idle, the
+    library's cached HIP events (aflex_teardown). Registered to run at
+    interpreter exit, so that no HIP object of ours is left for the runtime's
+    own teardown; the library stays usable afterwards (a later call re-creates
+    what it needs)."""
+    if _lib is None:
+        return
+    release_pool_streams()
+    if torch.cuda.is_initialized():
+        for d in range(torch.cuda.device_count()):
+            torch.cuda.synchronize(d)
+    _check(_lib.aflex_teardown())
 
 
 def profile_start(kernels=None):
@@ -354,7 +399,8 @@ _pool_streams = {}
 
 def pool_streams(attn_cus: int, device="cuda:0"):
     """Stream pair on disjoint CU sets (attn_cus of 256 CUs for the attention stage),
-    as torch external streams; created once per (device, attn_cus), kept for the process."""
+    as torch external streams; created once per (device, attn_cus) and destroyed
+    by release_pool_streams() (by close() at interpreter exit at the latest)."""
     d = torch.device(device)
     key = (d, attn_cus)
     if key not in _pool_streams:

@@ -9,6 +9,7 @@
 
 #include "aflex.h"
 #include "kernels.h"
+#include "profile.h"
 
 namespace {
 
@@ -293,7 +294,31 @@ aflex_status aflex_linear(const aflex_linear_args* l, void* ws, size_t ws_bytes,
   if (s != AFLEX_OK) return s;
   return hip_status(aflex::launch_linear(*l, ws, (hipStream_t)stream), "linear");
 }
-const char* aflex_version(void) { return "aflex 0.1 gfx950"; }
+const char* aflex_version(void) { return "aflex 0.2 gfx950"; }
+
+aflex_status aflex_teardown(void) {
+  hipError_t first = hipSuccess;
+  {
+    std::lock_guard<std::mutex> lock(g_events.mu);
+    int cur = 0;
+    const bool have_cur = hipGetDevice(&cur) == hipSuccess;
+    for (size_t dev = 0; dev < g_events.per_device.size(); ++dev) {
+      std::vector<hipEvent_t>& ev = g_events.per_device[dev];
+      if (ev.empty()) continue;
+      hipError_t e = hipSetDevice((int)dev);
+      for (hipEvent_t x : ev) {
+        const hipError_t r = hipEventDestroy(x);
+        if (e == hipSuccess) e = r;
+      }
+      ev.clear();
+      if (first == hipSuccess) first = e;
+    }
+    if (have_cur) (void)hipSetDevice(cur);
+  }
+  const hipError_t e = aflex::profile_release();
+  if (first == hipSuccess) first = e;
+  return hip_status(first, "teardown");
+}
 
 aflex_status aflex_attn_decode_workspace(const aflex_attn_args* a, size_t* bytes) {
   REQUIRE(bytes, AFLEX_ERR_INVALID_ARG, "attn: bytes is NULL");

@@ -7,6 +7,7 @@ namespace aflex {
 
 bool profile_wants(const char* name);
 void profile_mark(const char* name, hipStream_t stream, bool begin);
+hipError_t profile_release();
 
 struct ProfScope {
   const char* name;

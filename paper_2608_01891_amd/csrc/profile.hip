@@ -81,6 +81,29 @@ void profile_mark(const char* name, hipStream_t stream, bool begin) {
   }
 }
 
+// Destroys every event the profiler holds (records and the free list) and
+// ends an active session. The caller guarantees that no recorded event is
+// still pending on a stream.
+hipError_t profile_release() {
+  g_active.store(false);
+  std::lock_guard<std::mutex> lock(g_mu);
+  hipError_t first = hipSuccess;
+  auto destroy = [&](hipEvent_t e) {
+    if (!e) return;
+    const hipError_t r = hipEventDestroy(e);
+    if (first == hipSuccess) first = r;
+  };
+  for (auto& r : g_recs) {
+    destroy(r.start);
+    destroy(r.stop);
+  }
+  for (hipEvent_t e : g_free) destroy(e);
+  g_recs.clear();
+  g_free.clear();
+  g_open.clear();
+  return first;
+}
+
 }  // namespace aflex
 
 extern "C" {
