@@ -99,6 +99,7 @@ def load():
     sig = {
         "aflex_attn_decode_workspace": [AP, _SZ],
         "aflex_attn_decode": [AP, _p, ctypes.c_size_t, _p],
+        "aflex_attn_decode_noalloc": [AP, _p],
         "aflex_ffn_swiglu_workspace": [FP, _SZ],
         "aflex_ffn_swiglu": [FP, _p, ctypes.c_size_t, _p],
         "aflex_moe_ffn_workspace": [FP, _SZ],
@@ -266,6 +267,16 @@ def attn_decode(a, out=None, split_tokens: int = 0, scale: float = 0.0, stream=N
     _check(lib.aflex_attn_decode_workspace(ctypes.byref(args), ctypes.byref(n)))
     p, sz = _ws("attn", n.value, a.q.device, ws, (stream,))
     _check(lib.aflex_attn_decode(ctypes.byref(args), p, sz, _stream(stream)))
+    return out
+
+
+def attn_decode_noalloc(a, out, split_tokens: int = 0, scale: float = 0.0, stream=None):
+    """Decode attention into ``out`` without a workspace: the library's static
+    device scratch holds the split partials (calls on one device must not
+    overlap)."""
+    lib = load()
+    args = attn_args(a, out, split_tokens, scale)
+    _check(lib.aflex_attn_decode_noalloc(ctypes.byref(args), _stream(stream)))
     return out
 
 

@@ -336,6 +336,20 @@ aflex_status aflex_attn_decode(const aflex_attn_args* a, void* ws, size_t ws_byt
   return hip_status(aflex::launch_attn_decode(*a, ws, (hipStream_t)stream, true), "attn");
 }
 
+aflex_status aflex_attn_decode_noalloc(const aflex_attn_args* a, aflex_stream stream) {
+  aflex_status s = check_attn(a, true);
+  if (s != AFLEX_OK) return s;
+  const size_t need = aflex::attn_workspace_bytes(*a);
+  REQUIRE(need <= aflex::kStaticScratchBytes, AFLEX_ERR_WORKSPACE,
+          "attn_noalloc: this shape needs %zu bytes of scratch, the library's static scratch holds %zu "
+          "(lower B * Hq * ceil(max_context_len / split) or use aflex_attn_decode with a workspace)",
+          need, aflex::kStaticScratchBytes);
+  void* ws = nullptr;
+  hipError_t e = aflex::static_scratch(&ws);
+  if (e != hipSuccess) return hip_status(e, "attn_noalloc: static scratch");
+  return hip_status(aflex::launch_attn_decode(*a, ws, (hipStream_t)stream, true), "attn_noalloc");
+}
+
 aflex_status aflex_ffn_swiglu_workspace(const aflex_ffn_args* f, size_t* bytes) {
   REQUIRE(bytes, AFLEX_ERR_INVALID_ARG, "swiglu: bytes is NULL");
   aflex_status s = check_ffn(f, false, true);

@@ -9,6 +9,13 @@ namespace aflex {
 
 inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
+// Library-owned device scratch of the entry points that allocate nothing
+// (scratch.hip): kStaticScratchBytes per device, shared by every such call on
+// that device. static_scratch returns its device address on the current
+// device (looked up once per device, then cached).
+constexpr size_t kStaticScratchBytes = size_t(64) << 20;
+hipError_t static_scratch(void** ptr);
+
 // Decode attention (attn_decode.hip).
 int attn_split_tokens(const aflex_attn_args& a);
 size_t attn_workspace_bytes(const aflex_attn_args& a);

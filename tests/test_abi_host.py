@@ -21,7 +21,7 @@ def lib():
 
 def test_exports_every_declared_symbol(lib):
     names = aflex.exported_names()
-    assert len(names) == 22
+    assert len(names) == 23
     for n in names:
         assert hasattr(lib, n), n
     assert lib.aflex_version().startswith(b"aflex")
@@ -74,6 +74,17 @@ def _attn_status(lib, a, ws_bytes=1 << 40):
 def test_attention_rejects(lib, kw, status):
     assert _attn_status(lib, _attn(**kw)) == status
     assert lib.aflex_last_error()
+
+
+def test_attention_noalloc_rejects_before_launch(lib):
+    """The no-allocation attention validates like aflex_attn_decode and refuses
+    shapes whose split partials exceed its static scratch (64 MiB), on the host,
+    before any device call."""
+    a = _attn(q=None)
+    assert lib.aflex_attn_decode_noalloc(ctypes.byref(a), None) == aflex.ERR_INVALID_ARG
+    big = _attn(B=4096, Hq=64, Hkv=8, D=128, max_blocks_per_seq=2048, max_context_len=32768)
+    assert lib.aflex_attn_decode_noalloc(ctypes.byref(big), None) == aflex.ERR_WORKSPACE
+    assert b"static scratch" in lib.aflex_last_error()
 
 
 def test_attention_workspace(lib):
