@@ -316,7 +316,7 @@ def main():
     ms_step = (t1 - t0) * 1e3 / args.steps
 
     # same steps again with HIP events around the dominant kernel on its stream
-    STAGE_A = ("attn_split", "attn_merge")
+    STAGE_A = ("attn_decode", "attn_merge")
     STAGE_F = ("moe_route", DOMINANT, "gemm_down", "moe_combine")
     aflex.profile_start(list(STAGE_A + STAGE_F))
     t2 = time.perf_counter()
@@ -577,7 +577,7 @@ def main():
         wt = synth.tiny_layer(device=dev)
         ot = aflex.attn_decode(wt.attn)
         yt = aflex.ffn_swiglu(wt.x, wt.ffn)
-        ms_a, kk_a = timed_kernels(lambda: aflex.attn_decode(wt.attn, out=ot), 50, ["attn_split", "attn_merge"], aflex)
+        ms_a, kk_a = timed_kernels(lambda: aflex.attn_decode(wt.attn, out=ot), 50, ["attn_decode", "attn_merge"], aflex)
         ms_f, kk_f = timed_kernels(lambda: aflex.ffn_swiglu(wt.x, wt.ffn, y=yt), 50,
                                    ["gemm_gate_up", "gemm_down", "splitk_reduce"], aflex)
         ops["tiny_layer"] = {"attention_ms": round(ms_a, 5), "swiglu_ms": round(ms_f, 5),
@@ -600,7 +600,7 @@ def main():
             it[0] += 1
         for _ in range(3):
             run_attn()
-        ms, kk = timed_kernels(run_attn, 30, ["attn_split", "attn_merge"], aflex)
+        ms, kk = timed_kernels(run_attn, 30, ["attn_decode", "attn_merge"], aflex)
         ops["attention_qwen3_B64"] = {
             "ms": round(ms, 5), "GB_per_s": round(abytes / (ms * 1e-3) / 1e9, 1),
             "hbm_frac": round(abytes / (ms * 1e-3) / PEAK_HBM, 4), "bytes": abytes,
@@ -625,7 +625,7 @@ def main():
             it[0] += 1
         for _ in range(3):
             run_stage()
-        ms, kk = timed_kernels(run_stage, 30, ["kv_append", "attn_split", "attn_merge", "gemm_down", "splitk_reduce"], aflex)
+        ms, kk = timed_kernels(run_stage, 30, ["kv_append", "attn_decode", "attn_merge", "gemm_down", "splitk_reduce"], aflex)
         sbytes = abytes + w_o.numel() * 2 + 2 * wq.B * 5120 * 2 + 2 * kn.numel() * 2
         ops["attention_stage_qwen3_B64"] = {
             "ms": round(ms, 5), "GB_per_s": round(sbytes / (ms * 1e-3) / 1e9, 1),

@@ -84,13 +84,19 @@ typedef struct aflex_attn_args {
   int32_t max_context_len;     /* host-known bound on every ctx_b (<= max_blocks_per_seq*bs);
                                   sizes the launch grid, larger device values are clamped */
   float scale;                 /* softmax scale; 0 selects 1/sqrt(D) */
-  int32_t split_tokens;        /* tokens per work-group split; 0 selects the library default,
-                                  else a multiple of 128 in [128, 1024] */
+  int32_t split_tokens;        /* 0: the cached blocks of all (sequence, kv head) pairs are
+                                  spread evenly over the work-groups the GPU holds at once;
+                                  else each work-group takes this many tokens' blocks of them
+                                  (a multiple of 128 in [128, 1024]) */
 } aflex_attn_args;
 
 /* Supported: D in {64, 128}, block_size == 16, Hkv >= 1, Hq % Hkv == 0,
- * 1 <= Hq / Hkv <= 16. ctx_b == 0 yields out = 0. Block ids outside
- * [0, num_blocks) contribute nothing (their tokens are masked). */
+ * 1 <= Hq / Hkv <= 16, B * Hkv * ceil(max_context_len / 16) < 2^30.
+ * ctx_b == 0 yields out = 0. Block ids outside [0, num_blocks) contribute
+ * nothing (their tokens are masked). Two launches on the stream: the split
+ * attention, then a merge of the (sequence, kv head) pairs it split between
+ * work-groups; the workspace holds their fp32 partials and needs no
+ * initialisation. */
 aflex_status aflex_attn_decode_workspace(const aflex_attn_args *a, size_t *bytes);
 aflex_status aflex_attn_decode(const aflex_attn_args *a, void *workspace, size_t workspace_bytes,
                                aflex_stream stream);
@@ -301,8 +307,8 @@ aflex_status aflex_pool_streams_destroy(aflex_stream stream_a, aflex_stream stre
 /* aflex_profile_start and aflex_profile_stop, every library kernel whose     */
 /* name is in the comma-separated list `kernels` (NULL or "" = all) is        */
 /* bracketed by two HIP events on the stream it is launched on. Kernel names: */
-/* attn_split, attn_merge, gemm_gate_up, gemm_down, splitk_reduce, moe_route, */
-/* moe_combine, kv_append, kv_write, rmsnorm_router, attn_prefill.            */
+/* attn_decode, attn_merge, gemm_gate_up, gemm_down, splitk_reduce,          */
+/* moe_route, moe_combine, kv_append, kv_write, rmsnorm_router, attn_prefill. */
 /* aflex_profile_stop waits for those events and writes one line per kernel   */
 /* into `report` (host buffer of `len` bytes, truncated to fit):              */
 /*   <name> <launches> <total_ms> <min_ms> <max_ms>                           */

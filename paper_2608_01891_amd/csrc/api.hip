@@ -53,6 +53,8 @@ aflex_status check_attn(const aflex_attn_args* a, bool need_out) {
           AFLEX_ERR_INVALID_ARG, "attn: split_tokens %d must be 0 or a multiple of 128 in [128, 1024]",
           a->split_tokens);
   REQUIRE(isfinite(a->scale) && a->scale >= 0.f, AFLEX_ERR_INVALID_ARG, "attn: scale must be finite and >= 0");
+  REQUIRE(aflex::attn_shape_fits(*a), AFLEX_ERR_UNSUPPORTED,
+          "attn: B * Hkv * ceil(max_context_len / 16) must stay below 2^30");
   REQUIRE(aligned16(a->q) && aligned16(a->k_cache) && aligned16(a->v_cache) && (!a->out || aligned16(a->out)),
           AFLEX_ERR_ALIGNMENT, "attn: q, k_cache, v_cache and out must be 16-byte aligned");
   REQUIRE(((uintptr_t)a->block_table & 3u) == 0 && ((uintptr_t)a->context_lens & 3u) == 0, AFLEX_ERR_ALIGNMENT,

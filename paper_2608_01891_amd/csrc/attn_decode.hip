@@ -5,9 +5,18 @@
 // decode-step attention the paper treats as the memory-bound operator
 // (section 1; section 3.2).
 //
-// Design (HBM-bound: every cached K/V byte is read exactly once):
-//  * split kernel: one work-group of 4 waves per (sequence, kv head, split of
-//    split_tokens tokens). Waves take pairs of 16-token blocks round-robin.
+// Design (HBM-bound: every cached K/V byte is read exactly once, in one
+// launch):
+//  * Work partition. The (sequence, kv head) units are laid end to end in
+//    (b, kv head) order, each as its ceil(ctx_b / 16) blocks; work-group i of
+//    the grid takes blocks [i C, (i+1) C) of that flattened range, with C the
+//    range divided evenly over the grid (or a fixed size the caller asks
+//    for). Every work-group computes the partition itself from the context
+//    lengths (no host synchronisation, no extra launch), so all of them
+//    stream the same number of bytes and finish together; a work-group's
+//    range is one or more pieces, each the part of one unit that falls into
+//    it.
+//  * Piece kernel body: 4 waves take pairs of 16-token blocks round-robin.
 //    Per pair a wave issues 16 (D=128) 16-byte loads per lane straight into
 //    MFMA operand registers -- no LDS staging is needed because both
 //    contractions see their operand with the contraction index contiguous:
@@ -21,12 +30,19 @@
 //    registers of a lane are exactly the P^T operand registers it needs for
 //    the PV product, and all softmax state of head g lives in the four lanes
 //    with lane % 16 == g: the online softmax needs two cross-lane max steps per
-//    block pair and no LDS round trip.
-//  * the 4 waves of a work-group merge through LDS; a sequence with a single
-//    split writes bf16 output directly, longer ones write an fp32 partial
-//    (O, m, l) for the merge kernel.
-//  * merge kernel: one wave per (sequence, head) rescales and sums the splits.
+//    block pair and no LDS round trip. The 4 waves then merge through LDS.
+//  * Merge. A unit held by one piece writes its bf16 output directly. A unit
+//    cut into several pieces (consecutive work-groups; only the first and the
+//    last piece of a work-group's range can be such a piece) has each piece
+//    write an fp32 partial (O, m, l) to slot unit + work-group, unique over
+//    all pieces; a second, small launch merges the partials of those units in
+//    work-group order. Exchanging partials inside the first launch (flags or
+//    tickets between work-groups, each a round trip through the loaded
+//    memory system) stalled the work-groups that hold split units by several
+//    microseconds per exchange, more than the second launch costs.
 #include <math.h>
+
+#include <atomic>
 
 #include "common.h"
 #include "kernels.h"
@@ -41,20 +57,24 @@ struct AttnParams {
   const int32_t* bt;
   const int32_t* cl;
   uint16_t* out;
-  float* part_o;   // [B*Hq, max_splits, D]
-  float* part_ml;  // [B*Hq, max_splits, 2]  (running max in log2 units, sum)
+  float* part_o;                 // [U + P][G][D]
+  float* part_ml;                // [U + P][G][2]  (running max in log2 units, sum)
+  int2* span;                    // [U]  first and last work-group of each unit's pieces
   int B, Hq, Hkv, G;
   int max_blocks, num_blocks, max_ctx;
-  int split_tokens, max_splits;
-  float scale_log2;  // softmax scale * log2(e)
+  int chunk_blocks;              // > 0: fixed blocks per work-group; 0: even split over the grid
+  float scale_log2;              // softmax scale * log2(e)
 };
 
 constexpr int kWaves = 4;
+constexpr int kMinChunkBlocks = 8;  // one pair per wave at least
 
 __device__ __forceinline__ int clamp_ctx(const AttnParams& p, int b) {
   int c = p.cl[b];
   return c < 0 ? 0 : (c > p.max_ctx ? p.max_ctx : c);
 }
+
+__device__ __forceinline__ int nblk_of(int ctx) { return (ctx + 15) >> 4; }
 
 // K/V tile loads; NT marks them non-temporal (each cached byte is read once).
 template <bool NT>
@@ -67,8 +87,48 @@ __device__ __forceinline__ bf16x8 ld_kv(const uint16_t* ptr) {
   }
 }
 
+__device__ __forceinline__ int wave_sum_i(int v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+
+// Inclusive prefix sum over the 64 lanes of a wave.
+__device__ __forceinline__ int wave_incl_scan(int v, int lane) {
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int t = __shfl_up(v, o);
+    if (lane >= o) v += t;
+  }
+  return v;
+}
+
+// Block id of local block jb of sequence b's table, or -1 when jb is past the
+// piece's end or the table entry is out of range (its tokens are masked).
+__device__ __forceinline__ int load_block_id(const AttnParams& p, int b, int jb, int j_end) {
+  int id = -1;
+  if (jb < j_end) {
+    id = p.bt[(size_t)b * p.max_blocks + jb];
+    if (id < 0 || id >= p.num_blocks) id = -1;
+  }
+  return id;
+}
+
+// Partition of the flattened block range, as the decode kernel computes it:
+// per kv head the blocks of all sequences (total) and blocks per work-group.
+__device__ __forceinline__ int chunk_of(const AttnParams& p, int P, int lane, int* W_out) {
+  int total = 0;
+  for (int c = 0; c < p.B; c += 64) {
+    const int b = c + lane;
+    total += wave_sum_i(b < p.B ? nblk_of(clamp_ctx(p, b)) : 0);
+  }
+  const int W = __builtin_amdgcn_readfirstlane(total) * p.Hkv;
+  *W_out = W;
+  return p.chunk_blocks ? p.chunk_blocks : max((W + P - 1) / P, kMinChunkBlocks);
+}
+
 template <int D, bool NT>
-__global__ __launch_bounds__(256, 2) void attn_split_kernel(AttnParams p) {
+__global__ __launch_bounds__(256, 3) void attn_decode_kernel(AttnParams p) {
   constexpr int NC = D / 32;   // k-chunks of the QK product
   constexpr int NMT = D / 16;  // d-tiles of the PV product
   constexpr int LDO = D + 4;   // padded row of the LDS merge buffer
@@ -76,42 +136,53 @@ __global__ __launch_bounds__(256, 2) void attn_split_kernel(AttnParams p) {
   __shared__ float sm_ml[kWaves][2][16];
   __shared__ __attribute__((aligned(16))) float sm_o[kWaves][16][LDO];
 
-  const int bh = blockIdx.x;
-  const int b = bh / p.Hkv;
-  const int kvh = bh - b * p.Hkv;
-  const int split = blockIdx.y;
-  const int ctx = clamp_ctx(p, b);
-  const int S = p.split_tokens;
-  const int t0 = split * S;
-  if (t0 > 0 && t0 >= ctx) return;  // split 0 always runs (it writes zeros when ctx == 0)
-  const int t1 = min(t0 + S, ctx);
-  const int nsplit = max(1, (ctx + S - 1) / S);
-  const int jb0 = t0 / 16;
-  const int nblk = (t1 - t0 + 15) / 16;
-  const int npairs = (nblk + 1) / 2;
-
   const int tid = threadIdx.x;
   const int wave = tid >> 6;
   const int lane = tid & 63;
   const int r = lane & 15;   // MFMA row/col within the 16-wide tile
   const int qg = lane >> 4;  // lane group: which 8-wide k slice the lane feeds
   const int G = p.G;
-  const int h0 = kvh * G;
+  const int Hkv = p.Hkv;
+  const int wg = blockIdx.x;
+  const int P = gridDim.x;
 
-  // Physical block ids of this split: lane i holds entry jb0 + i (split <= 64 blocks).
-  int my_id = -1;
-  if (lane < nblk) {
-    my_id = p.bt[(size_t)b * p.max_blocks + jb0 + lane];
-    if (my_id < 0 || my_id >= p.num_blocks) my_id = -1;
+  // Sequences with no cached token produce zeros; work-group wg clears those
+  // with b = wg (mod P).
+  for (int b = wg; b < p.B; b += P) {
+    if (clamp_ctx(p, b) == 0) {
+      uint4* o = reinterpret_cast<uint4*>(p.out + (size_t)b * p.Hq * D);
+      for (int i = tid; i < p.Hq * D / 8; i += 256) o[i] = make_uint4(0, 0, 0, 0);
+    }
   }
 
-  // q as the B operand of the QK product: column g = r, k = d in [c*32 + qg*8, +8).
-  bf16x8 qf[NC];
-#pragma unroll
-  for (int c = 0; c < NC; ++c) {
-    qf[c] = (r < G) ? ld_bf16x8(p.q + ((size_t)b * p.Hq + h0 + r) * D + c * 32 + qg * 8)
-                    : zero_bf16x8();
+  // ---- partition: this work-group's range of the flattened blocks ----
+  int W;
+  const int C = chunk_of(p, P, lane, &W);
+  const int x0 = wg * C;
+  if (x0 >= W) return;
+  const int x1 = min(x0 + C, W);
+
+  // First sequence whose blocks reach past x0: base = its first block position
+  // per kv head (x positions are base * Hkv + kvh * nblk + j).
+  int b = 0, base = 0;
+  for (int c = 0; c < p.B; c += 64) {
+    const int bb = c + lane;
+    const int n = bb < p.B ? nblk_of(clamp_ctx(p, bb)) : 0;
+    const int incl = wave_incl_scan(n, lane);
+    const unsigned long long past = __ballot((base + incl) * Hkv > x0);
+    if (past) {
+      const int l = __builtin_ctzll(past);
+      b = c + l;
+      base += __builtin_amdgcn_readlane(incl - n, l);
+      break;
+    }
+    base += __builtin_amdgcn_readlane(incl, 63);
   }
+  // (every value that steers the piece loop is wave-uniform: scalar registers)
+  b = __builtin_amdgcn_readfirstlane(b);
+  base = __builtin_amdgcn_readfirstlane(base);
+  int nb = nblk_of(clamp_ctx(p, b));
+  int kvh = (x0 - base * Hkv) / nb;
 
   // Token slots. QK tile row rr (lane rr loads it) holds token
   //   block (rr >> 3), offset ((rr >> 2) & 1) * 8 + (rr & 3)    [first product]
@@ -124,204 +195,276 @@ __global__ __launch_bounds__(256, 2) void attn_split_kernel(AttnParams p) {
   const int vsel = qg >> 1;
   const int vtok = (qg & 1) * 8;
 
-  float m_run = kNegInf;
-  float l_run = 0.f;
-  f32x4 acc[NMT];
-#pragma unroll
-  for (int mt = 0; mt < NMT; ++mt) acc[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  int rot = 0;  // wave that takes the piece's first pair: spreads the odd pairs over the waves
 
-  for (int pr = wave; pr < npairs; pr += kWaves) {
-    const int idA = __builtin_amdgcn_readlane(my_id, 2 * pr);
-    const int idB = __builtin_amdgcn_readlane(my_id, 2 * pr + 1);
-    const int tA = (jb0 + 2 * pr) * 16;
+  int x = x0;
+  // First block-id chunk of the current piece; each piece loads the next
+  // piece's first chunk while it streams, so a new piece starts with its K/V
+  // loads instead of a round trip for its block ids.
+  int piece_ids = load_block_id(p, b, x0 - (base * Hkv + kvh * nb) + lane, min(nb, x1 - (base * Hkv + kvh * nb)));
+  while (x < x1) {
+    const int ctx = clamp_ctx(p, b);
+    const int ustart = base * Hkv + kvh * nb;  // position of the unit's first block
+    const int j0 = x - ustart;
+    const int j1 = min(nb, x1 - ustart);
+    const int h0 = kvh * G;
+    const int npairs = (j1 - j0 + 1) / 2;
 
-    bf16x8 k1[NC], k2[NC], vf[NMT];
-    const int pk = ksel ? idB : idA;
-    if (pk >= 0) {
-      const uint16_t* kb = p.kc + ((size_t)pk * p.Hkv + kvh) * 16 * D + qg * 8;
-#pragma unroll
-      for (int c = 0; c < NC; ++c) {
-        k1[c] = ld_kv<NT>(kb + ktok * D + c * 32);
-        k2[c] = ld_kv<NT>(kb + (ktok + 4) * D + c * 32);
-      }
-    } else {
-#pragma unroll
-      for (int c = 0; c < NC; ++c) k1[c] = k2[c] = zero_bf16x8();
+    // The next piece (it starts at its unit's first block): the next kv head
+    // of b, else the next sequence with blocks.
+    const int xn = ustart + j1;
+    int bn = b, kvhn = kvh + 1, basen = base, nbn = nb;
+    if (kvhn == Hkv) {
+      kvhn = 0;
+      basen = base + nb;
+      do {
+        ++bn;
+      } while (xn < x1 && bn < p.B && nblk_of(clamp_ctx(p, bn)) == 0);
+      nbn = (xn < x1) ? nblk_of(clamp_ctx(p, bn)) : 0;
     }
-    const int pv = vsel ? idB : idA;
-    const int tb = tA + vsel * 16 + vtok;  // first token of this lane's 8-token slice
-    const int nv = (pv >= 0) ? ctx - tb : 0;
-    if (pv >= 0) {
-      const uint16_t* vb = p.vc + ((size_t)pv * p.Hkv + kvh) * D * 16 + vtok;
-#pragma unroll
-      for (int mt = 0; mt < NMT; ++mt) vf[mt] = ld_kv<NT>(vb + (mt * 16 + r) * 16);
-    } else {
-#pragma unroll
-      for (int mt = 0; mt < NMT; ++mt) vf[mt] = zero_bf16x8();
-    }
-    if (nv < 8) {  // tail of the last block (or a skipped block): zero V so 0 * NaN cannot leak
-#pragma unroll
-      for (int mt = 0; mt < NMT; ++mt) vf[mt] = keep_first(vf[mt], nv);
-    }
+    const int next_piece_ids = (xn < x1) ? load_block_id(p, bn, lane, min(nbn, x1 - xn)) : -1;
 
-    f32x4 s1 = {0.f, 0.f, 0.f, 0.f}, s2 = {0.f, 0.f, 0.f, 0.f};
+    // q as the B operand of the QK product: column g = r, k = d in [c*32 + qg*8, +8).
+    bf16x8 qf[NC];
 #pragma unroll
     for (int c = 0; c < NC; ++c) {
-      s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k1[c], qf[c], s1, 0, 0, 0);
-      s2 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k2[c], qf[c], s2, 0, 0, 0);
+      qf[c] = (r < G) ? ld_bf16x8(p.q + ((size_t)b * p.Hq + h0 + r) * D + c * 32 + qg * 8)
+                      : zero_bf16x8();
     }
 
-    float sv[8];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      sv[i] = (i < nv) ? s1[i] * p.scale_log2 : kNegInf;
-      sv[4 + i] = (4 + i < nv) ? s2[i] * p.scale_log2 : kNegInf;
-    }
-    float mx = sv[0];
-#pragma unroll
-    for (int i = 1; i < 8; ++i) mx = fmaxf(mx, sv[i]);
-    mx = fmaxf(mx, __shfl_xor(mx, 16));
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
-    const float m_new = fmaxf(m_run, mx);
-    const float m_use = (m_new == kNegInf) ? 0.f : m_new;
-    const float alpha = fast_exp2(m_run - m_use);
-    bf16x8 pb;
-    float ps = 0.f;
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const __bf16 e = static_cast<__bf16>(fast_exp2(sv[i] - m_use));
-      pb[i] = e;
-      ps += static_cast<float>(e);
-    }
-    l_run = l_run * alpha + ps;
-    m_run = m_new;
-#pragma unroll
-    for (int mt = 0; mt < NMT; ++mt) {
-      acc[mt] *= alpha;
-      acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf[mt], pb, acc[mt], 0, 0, 0);
-    }
-  }
+    // Block ids of the piece, 64 per wave register (lane l: local block
+    // j0 + 64 c + l of chunk c); the next chunk is loaded one chunk ahead.
+    int my_id = piece_ids;
+    int next_id = (npairs > 32) ? load_block_id(p, b, j0 + 64 + lane, j1) : -1;
+    int cur_chunk = 0;
 
-  // Sum of the softmax denominators over the 4 lanes that share head g.
-  l_run += __shfl_xor(l_run, 16);
-  l_run += __shfl_xor(l_run, 32);
+    float m_run = kNegInf;
+    float l_run = 0.f;
+    f32x4 acc[NMT];
+#pragma unroll
+    for (int mt = 0; mt < NMT; ++mt) acc[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  if (qg == 0) {
-    sm_ml[wave][0][r] = m_run;
-    sm_ml[wave][1][r] = l_run;
-  }
-#pragma unroll
-  for (int mt = 0; mt < NMT; ++mt)
-    *reinterpret_cast<f32x4*>(&sm_o[wave][r][mt * 16 + 4 * qg]) = acc[mt];
-  __syncthreads();
+    for (int pr = (wave - rot) & (kWaves - 1); pr < npairs; pr += kWaves) {
+      if ((pr >> 5) != cur_chunk) {  // advances by at most one chunk per step
+        cur_chunk = pr >> 5;
+        my_id = next_id;
+        next_id = ((cur_chunk + 1) * 32 < npairs) ? load_block_id(p, b, j0 + (cur_chunk + 1) * 64 + lane, j1) : -1;
+      }
+      const int idA = __builtin_amdgcn_readlane(my_id, (2 * pr) & 63);
+      const int idB = __builtin_amdgcn_readlane(my_id, (2 * pr + 1) & 63);
+      const int tA = (j0 + 2 * pr) * 16;
 
-  for (int it = tid; it < G * D; it += 256) {
-    const int g = it / D;
-    const int d = it - g * D;
-    float M = sm_ml[0][0][g];
+      bf16x8 k1[NC], k2[NC], vf[NMT];
+      const int pk = ksel ? idB : idA;
+      if (pk >= 0) {
+        const uint16_t* kb = p.kc + ((size_t)pk * Hkv + kvh) * 16 * D + qg * 8;
 #pragma unroll
-    for (int w = 1; w < kWaves; ++w) M = fmaxf(M, sm_ml[w][0][g]);
-    const float Mu = (M == kNegInf) ? 0.f : M;
-    float L = 0.f, O = 0.f;
+        for (int c = 0; c < NC; ++c) {
+          k1[c] = ld_kv<NT>(kb + ktok * D + c * 32);
+          k2[c] = ld_kv<NT>(kb + (ktok + 4) * D + c * 32);
+        }
+      } else {
 #pragma unroll
-    for (int w = 0; w < kWaves; ++w) {
-      const float wt = fast_exp2(sm_ml[w][0][g] - Mu);
-      L += wt * sm_ml[w][1][g];
-      O += wt * sm_o[w][g][d];
-    }
-    const size_t row = (size_t)b * p.Hq + h0 + g;
-    if (nsplit == 1) {
-      p.out[row * D + d] = f2bf(L > 0.f ? O / L : 0.f);
-    } else {
-      const size_t prow = row * p.max_splits + split;
-      p.part_o[prow * D + d] = O;
-      if (d == 0) {
-        p.part_ml[prow * 2 + 0] = M;
-        p.part_ml[prow * 2 + 1] = L;
+        for (int c = 0; c < NC; ++c) k1[c] = k2[c] = zero_bf16x8();
+      }
+      const int pv = vsel ? idB : idA;
+      const int tb = tA + vsel * 16 + vtok;  // first token of this lane's 8-token slice
+      const int nv = (pv >= 0) ? ctx - tb : 0;
+      if (pv >= 0) {
+        const uint16_t* vb = p.vc + ((size_t)pv * Hkv + kvh) * D * 16 + vtok;
+#pragma unroll
+        for (int mt = 0; mt < NMT; ++mt) vf[mt] = ld_kv<NT>(vb + (mt * 16 + r) * 16);
+      } else {
+#pragma unroll
+        for (int mt = 0; mt < NMT; ++mt) vf[mt] = zero_bf16x8();
+      }
+      if (nv < 8) {  // tail of the last block (or a skipped block): zero V so 0 * NaN cannot leak
+#pragma unroll
+        for (int mt = 0; mt < NMT; ++mt) vf[mt] = keep_first(vf[mt], nv);
+      }
+
+      f32x4 s1 = {0.f, 0.f, 0.f, 0.f}, s2 = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int c = 0; c < NC; ++c) {
+        s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k1[c], qf[c], s1, 0, 0, 0);
+        s2 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k2[c], qf[c], s2, 0, 0, 0);
+      }
+
+      float sv[8];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        sv[i] = (i < nv) ? s1[i] * p.scale_log2 : kNegInf;
+        sv[4 + i] = (4 + i < nv) ? s2[i] * p.scale_log2 : kNegInf;
+      }
+      float mx = sv[0];
+#pragma unroll
+      for (int i = 1; i < 8; ++i) mx = fmaxf(mx, sv[i]);
+      mx = fmaxf(mx, __shfl_xor(mx, 16));
+      mx = fmaxf(mx, __shfl_xor(mx, 32));
+      const float m_new = fmaxf(m_run, mx);
+      const float m_use = (m_new == kNegInf) ? 0.f : m_new;
+      const float alpha = fast_exp2(m_run - m_use);
+      bf16x8 pb;
+      float ps = 0.f;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const __bf16 e = static_cast<__bf16>(fast_exp2(sv[i] - m_use));
+        pb[i] = e;
+        ps += static_cast<float>(e);
+      }
+      l_run = l_run * alpha + ps;
+      m_run = m_new;
+#pragma unroll
+      for (int mt = 0; mt < NMT; ++mt) {
+        acc[mt] *= alpha;
+        acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf[mt], pb, acc[mt], 0, 0, 0);
       }
     }
+
+    // Sum of the softmax denominators over the 4 lanes that share head g.
+    l_run += __shfl_xor(l_run, 16);
+    l_run += __shfl_xor(l_run, 32);
+
+    __syncthreads();  // the previous piece's readers of the LDS buffers are done
+    if (qg == 0) {
+      sm_ml[wave][0][r] = m_run;
+      sm_ml[wave][1][r] = l_run;
+    }
+#pragma unroll
+    for (int mt = 0; mt < NMT; ++mt)
+      *reinterpret_cast<f32x4*>(&sm_o[wave][r][mt * 16 + 4 * qg]) = acc[mt];
+    __syncthreads();
+
+    // Work-groups holding pieces of this unit; the one with its first piece
+    // records the span for the merge launch.
+    const int wg_first = ustart / C;
+    const int wg_last = (ustart + nb - 1) / C;
+    const int unit = b * Hkv + kvh;
+    const size_t seg = (size_t)unit + wg;
+    if (tid == 0 && wg == wg_first) p.span[unit] = make_int2(wg_first, wg_last);
+
+    for (int it = tid; it < G * D; it += 256) {
+      const int g = it / D;
+      const int d = it - g * D;
+      float M = sm_ml[0][0][g];
+#pragma unroll
+      for (int w = 1; w < kWaves; ++w) M = fmaxf(M, sm_ml[w][0][g]);
+      const float Mu = (M == kNegInf) ? 0.f : M;
+      float L = 0.f, O = 0.f;
+#pragma unroll
+      for (int w = 0; w < kWaves; ++w) {
+        const float wt = fast_exp2(sm_ml[w][0][g] - Mu);
+        L += wt * sm_ml[w][1][g];
+        O += wt * sm_o[w][g][d];
+      }
+      if (wg_first == wg_last) {
+        p.out[((size_t)b * p.Hq + h0 + g) * D + d] = f2bf(L > 0.f ? O / L : 0.f);
+      } else {
+        p.part_o[(seg * G + g) * D + d] = O;
+        if (d == 0) {
+          p.part_ml[(seg * G + g) * 2 + 0] = M;
+          p.part_ml[(seg * G + g) * 2 + 1] = L;
+        }
+      }
+    }
+
+    rot = (rot + npairs) & (kWaves - 1);
+
+    x = xn;
+    b = bn;
+    kvh = kvhn;
+    base = basen;
+    nb = nbn;
+    piece_ids = next_piece_ids;
   }
 }
 
-__device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
-  return v;
-}
-
-__device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o);
-  return v;
-}
-
-// One wave per (sequence, head). Lanes first reduce the split maxima and
-// denominators in parallel, then each lane sums 4 consecutive d of every
-// NG-th split (NG = 64 / (D/4) lane groups) with 16-byte loads, and the groups
-// are combined with xor shuffles; the summation order is fixed.
+// Merge launch: work-group u merges unit u (sequence b = u / Hkv, kv head
+// u % Hkv) if the decode launch split it between work-groups (the span its
+// first piece recorded); each thread combines 4 consecutive d of one head
+// over the pieces in work-group order.
 template <int D>
 __global__ __launch_bounds__(256) void attn_merge_kernel(AttnParams p) {
   constexpr int D4 = D / 4;
-  constexpr int NG = 64 / D4;
-  const int wave = threadIdx.x >> 6;
-  const int lane = threadIdx.x & 63;
-  const int row = blockIdx.x * kWaves + wave;  // (b, h)
-  if (row >= p.B * p.Hq) return;
-  const int b = row / p.Hq;
-  const int ctx = clamp_ctx(p, b);
-  const int nsplit = (ctx + p.split_tokens - 1) / p.split_tokens;
-  if (nsplit <= 1) return;  // written by the split kernel
-  const float* ml = p.part_ml + (size_t)row * p.max_splits * 2;
-  float M = kNegInf;
-  for (int s = lane; s < nsplit; s += 64) M = fmaxf(M, ml[2 * s]);
-  M = wave_max(M);
-  const float Mu = (M == kNegInf) ? 0.f : M;
-  float L = 0.f;
-  for (int s = lane; s < nsplit; s += 64) L += fast_exp2(ml[2 * s] - Mu) * ml[2 * s + 1];
-  L = wave_sum(L);
-  const float inv = L > 0.f ? 1.f / L : 0.f;
-  const int grp = lane / D4, d4 = lane - grp * D4;
-  const float* po = p.part_o + (size_t)row * p.max_splits * D + d4 * 4;
-  f32x4 O = {0.f, 0.f, 0.f, 0.f};
+  const int unit = blockIdx.x;
+  const int b = unit / p.Hkv, kvh = unit - b * p.Hkv;
+  if (clamp_ctx(p, b) == 0) return;  // no piece, no recorded span
+  const int2 sp = p.span[unit];
+  const int wf = sp.x, wl = sp.y;
+  if (wf == wl) return;  // written by the decode launch
+  const int G = p.G;
+  for (int it = threadIdx.x; it < G * D4; it += 256) {
+    const int g = it / D4;
+    const int d4 = it - g * D4;
+    float M = kNegInf;
 #pragma unroll 4
-  for (int s = grp; s < nsplit; s += NG) O += fast_exp2(ml[2 * s] - Mu) * *reinterpret_cast<const f32x4*>(po + (size_t)s * D);
-#pragma unroll
-  for (int o = D4; o < 64; o <<= 1) {
-#pragma unroll
-    for (int e = 0; e < 4; ++e) O[e] += __shfl_xor(O[e], o);
-  }
-  if (grp == 0) {
+    for (int w = wf; w <= wl; ++w) M = fmaxf(M, p.part_ml[(((size_t)unit + w) * G + g) * 2]);
+    const float Mu = (M == kNegInf) ? 0.f : M;
+    float L = 0.f;
+    f32x4 O = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll 4
+    for (int w = wf; w <= wl; ++w) {
+      const size_t s = (size_t)unit + w;
+      const float wt = fast_exp2(p.part_ml[(s * G + g) * 2] - Mu);
+      L += wt * p.part_ml[(s * G + g) * 2 + 1];
+      O += wt * *reinterpret_cast<const f32x4*>(&p.part_o[(s * G + g) * D + d4 * 4]);
+    }
+    const float inv = L > 0.f ? 1.f / L : 0.f;
     ushort4 v;
     v.x = f2bf(O[0] * inv);
     v.y = f2bf(O[1] * inv);
     v.z = f2bf(O[2] * inv);
     v.w = f2bf(O[3] * inv);
-    *reinterpret_cast<ushort4*>(p.out + (size_t)row * D + d4 * 4) = v;
+    *reinterpret_cast<ushort4*>(p.out + ((size_t)b * p.Hq + kvh * G + g) * D + d4 * 4) = v;
   }
 }
 
-int attn_split_tokens(const aflex_attn_args& a) {
-  if (a.split_tokens > 0) return a.split_tokens;
-  // Longer splits amortise each work-group's fixed cost (the block-id and q
-  // loads ahead of its first K/V byte, the LDS merge, the partial write and
-  // the merge kernel's share) but leave fewer work-groups to fill 256 CUs.
-  // The context lengths stay on the device, so the work-group count is
-  // bounded through max_context_len: the longest split whose bound still
-  // leaves several rounds of work-groups.
-  const long kv_rows = (long)a.B * a.Hkv;
-  if (kv_rows * ((a.max_context_len + 1023) / 1024) >= 8192) return 1024;
-  return kv_rows * ((a.max_context_len + 511) / 512) >= 4096 ? 512 : 256;
+// ---------------------------------------------------------------------------
+// Host side.
+
+// Work-groups resident at once: three 4-wave work-groups per CU (the kernel's
+// register budget allows three waves per SIMD; two or four per CU measured
+// slower on the Qwen3-32B B = 64 workload: 69.9 and 75.4 against 65.5 us).
+static int resident_wgs() {
+  static std::atomic<int> cached{0};
+  int v = cached.load(std::memory_order_relaxed);
+  if (v > 0) return v;
+  int dev = 0, ncu = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || ncu <= 0)
+    ncu = 256;
+  v = 3 * ncu;
+  cached.store(v, std::memory_order_relaxed);
+  return v;
 }
 
-static int max_splits_of(const aflex_attn_args& a, int S) {
-  return a.max_context_len > 0 ? (a.max_context_len + S - 1) / S : 1;
+static long long work_bound(const aflex_attn_args& a) {
+  return (long long)a.B * a.Hkv * ((a.max_context_len + 15) / 16);
 }
+
+// Grid size: with a fixed piece size, enough work-groups for the bound on the
+// blocks; otherwise the resident work-groups, fewer when the bound cannot give
+// each of them a pair per wave.
+static int attn_grid(const aflex_attn_args& a) {
+  const long long wb = work_bound(a);
+  long long P;
+  if (a.split_tokens > 0) {
+    P = (wb + a.split_tokens / 16 - 1) / (a.split_tokens / 16);
+  } else {
+    P = (wb + kMinChunkBlocks - 1) / kMinChunkBlocks;
+    P = P < resident_wgs() ? P : resident_wgs();
+  }
+  return (int)(P < 1 ? 1 : P);
+}
+
+bool attn_shape_fits(const aflex_attn_args& a) { return work_bound(a) < (1ll << 30); }
 
 size_t attn_workspace_bytes(const aflex_attn_args& a) {
-  const int S = attn_split_tokens(a);
-  const size_t rows = (size_t)a.B * a.Hq * max_splits_of(a, S);
-  if (max_splits_of(a, S) <= 1) return 256;
-  return align_up(rows * a.D * sizeof(float), 256) + align_up(rows * 2 * sizeof(float), 256);
+  const size_t U = (size_t)a.B * a.Hkv;
+  const size_t segs = U + (size_t)attn_grid(a);
+  const size_t G = (size_t)(a.Hq / a.Hkv);
+  return align_up(segs * G * a.D * sizeof(float), 256) + align_up(segs * G * 2 * sizeof(float), 256) +
+         align_up(U * sizeof(int2), 256);
 }
 
 hipError_t launch_attn_decode(const aflex_attn_args& a, void* ws, hipStream_t stream, bool nt_kv) {
@@ -339,36 +482,39 @@ hipError_t launch_attn_decode(const aflex_attn_args& a, void* ws, hipStream_t st
   p.max_blocks = a.max_blocks_per_seq;
   p.num_blocks = a.num_blocks;
   p.max_ctx = a.max_context_len;
-  p.split_tokens = attn_split_tokens(a);
-  p.max_splits = max_splits_of(a, p.split_tokens);
+  p.chunk_blocks = a.split_tokens > 0 ? a.split_tokens / 16 : 0;
   const float scale = a.scale != 0.f ? a.scale : 1.0f / sqrtf((float)a.D);
   p.scale_log2 = scale * kLog2e;
-  const size_t rows = (size_t)a.B * a.Hq * p.max_splits;
-  p.part_o = static_cast<float*>(ws);
-  p.part_ml = reinterpret_cast<float*>(static_cast<char*>(ws) +
-                                       align_up(rows * a.D * sizeof(float), 256));
-  dim3 grid(a.B * a.Hkv, p.max_splits);
-  const unsigned merge_grid = (a.B * a.Hq + kWaves - 1) / kWaves;
+  const int P = attn_grid(a);
+  const size_t U = (size_t)a.B * a.Hkv;
+  const size_t segs = U + (size_t)P;
+  const size_t G = (size_t)p.G;
+  char* w = static_cast<char*>(ws);
+  p.part_o = reinterpret_cast<float*>(w);
+  w += align_up(segs * G * a.D * sizeof(float), 256);
+  p.part_ml = reinterpret_cast<float*>(w);
+  w += align_up(segs * G * 2 * sizeof(float), 256);
+  p.span = reinterpret_cast<int2*>(w);
   {
-    ProfScope ps("attn_split", stream);
+    ProfScope ps("attn_decode", stream);
     if (a.D == 128) {
       if (nt_kv)
-        attn_split_kernel<128, true><<<grid, 256, 0, stream>>>(p);
+        attn_decode_kernel<128, true><<<P, 256, 0, stream>>>(p);
       else
-        attn_split_kernel<128, false><<<grid, 256, 0, stream>>>(p);
+        attn_decode_kernel<128, false><<<P, 256, 0, stream>>>(p);
     } else {
       if (nt_kv)
-        attn_split_kernel<64, true><<<grid, 256, 0, stream>>>(p);
+        attn_decode_kernel<64, true><<<P, 256, 0, stream>>>(p);
       else
-        attn_split_kernel<64, false><<<grid, 256, 0, stream>>>(p);
+        attn_decode_kernel<64, false><<<P, 256, 0, stream>>>(p);
     }
   }
-  if (p.max_splits > 1) {
+  if (P > 1) {  // with one work-group no unit is split
     ProfScope ps("attn_merge", stream);
     if (a.D == 128)
-      attn_merge_kernel<128><<<merge_grid, 256, 0, stream>>>(p);
+      attn_merge_kernel<128><<<a.B * a.Hkv, 256, 0, stream>>>(p);
     else
-      attn_merge_kernel<64><<<merge_grid, 256, 0, stream>>>(p);
+      attn_merge_kernel<64><<<a.B * a.Hkv, 256, 0, stream>>>(p);
   }
   return hipGetLastError();
 }

@@ -16,8 +16,9 @@ inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 constexpr size_t kStaticScratchBytes = size_t(64) << 20;
 hipError_t static_scratch(void** ptr);
 
-// Decode attention (attn_decode.hip).
-int attn_split_tokens(const aflex_attn_args& a);
+// Decode attention (attn_decode.hip). attn_shape_fits: the flattened block
+// range B * Hkv * ceil(max_context_len / 16) stays below 2^30.
+bool attn_shape_fits(const aflex_attn_args& a);
 size_t attn_workspace_bytes(const aflex_attn_args& a);
 // nt_kv: stream the K/V tiles with non-temporal loads. Decode attention on its
 // own (an attention pool) reads each cached byte once and measured 2-4% faster
