@@ -101,20 +101,21 @@ aflex_status aflex_attn_decode_workspace(const aflex_attn_args *a, size_t *bytes
 aflex_status aflex_attn_decode(const aflex_attn_args *a, void *workspace, size_t workspace_bytes,
                                aflex_stream stream);
 
-/* Decode attention that allocates nothing, for callers that cannot call     */
+/* Decode attention that allocates nothing, for callers that cannot call      */
 /* hipMalloc or hand over a workspace: code under HIP graph capture, tight    */
-/* serving loops, harnesses that forbid allocation. Same operation,          */
-/* arguments, validation and result as aflex_attn_decode (the same kernels); */
-/* its split partials live in a static device array of the library, 64 MiB  */
-/* per device (held from the library's load on that device until the process */
-/* ends). Shapes whose partials need more (the aflex_attn_decode_workspace   */
-/* size, about B * Hq * ceil(max_context_len / split) * (D + 2) * 4 bytes)   */
-/* return AFLEX_ERR_WORKSPACE before anything is launched. Every call on a   */
-/* device shares that device's array: calls that may overlap on one device   */
-/* (different streams without ordering, several host threads) race and give */
-/* wrong results; order them on one stream. No HIP allocation, memset or     */
-/* host synchronisation happens in the call; the first call on a device      */
-/* looks up the array's device address (hipGetSymbolAddress) once.           */
+/* serving loops, harnesses that forbid allocation. Same operation,           */
+/* arguments, validation and result as aflex_attn_decode (the same kernels);  */
+/* its split partials live in a static device array of the library, 64 MiB    */
+/* per device (held from the library's load on that device until the process  */
+/* ends). Shapes whose partials need more (the aflex_attn_decode_workspace    */
+/* size, about (B * Hkv + 768) * (Hq / Hkv) * (D + 2) * 4 bytes on a 256-CU   */
+/* device with split_tokens = 0) return AFLEX_ERR_WORKSPACE before anything   */
+/* is launched. Every call on a device shares that device's array: calls that */
+/* may overlap on one device (different streams without ordering, several     */
+/* host threads) race and give wrong results; order them on one stream. No    */
+/* HIP allocation, memset or host synchronisation happens in the call; the    */
+/* first call on a device looks up the array's device address                 */
+/* (hipGetSymbolAddress) once.                                                */
 aflex_status aflex_attn_decode_noalloc(const aflex_attn_args *a, aflex_stream stream);
 
 /* ------------------------------------------------------------------------ */
