@@ -572,6 +572,39 @@ def main():
         aflex.release_pool_streams()
         ops["af_pipeline"] = variants
 
+        # The whole decode layer on the two streams (section 4.3): KV append,
+        # attention and output projection (+ the layer input) on the attention
+        # stream, RMSNorm, router, experts and residual on the FFN stream. The
+        # append writes each sequence's new token into the workload's pools
+        # (the same draws' shapes; later sections only time kernels on them).
+        lw = synth.make_layer(40, B, a.Hq, a.Hkv, a.D, H, f.E, device=dev)
+        ly = torch.empty(B, H, dtype=torch.bfloat16, device=dev)
+        lws = aflex.Workspace()
+        layer_ops = {}
+        for M in (1, 4):
+            m = plan.equal_microbatches(B, M)
+
+            def lstep():
+                aflex.af_layer_step(a, f, lw, k, m, y=ly, stream_a=sa, stream_f=sf, ws=lws, join=False)
+            lstep()
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            for _ in range(args.steps):
+                lstep()
+            torch.cuda.synchronize()
+            ms = (time.perf_counter() - t0) * 1e3 / args.steps
+            # algorithmic bytes: the pipeline step's, plus W_o once per
+            # microbatch, the router and norm weights, the layer input, h and y
+            lbytes = (step_bytes if M == 4 else kv_bytes_total + 8 * w_bytes_expert + B * H * 4) \
+                + M * (lw.w_o.numel() * 2 + lw.router_weight.numel() * 2 + H * 2) + 3 * B * H * 2
+            layer_ops[f"M={M}"] = {"ms": round(ms, 4), "tok_per_s": round(B / (ms * 1e-3), 1),
+                                   "GB_per_s": round(lbytes / (ms * 1e-3) / 1e9, 1),
+                                   "hbm_frac": round(lbytes / (ms * 1e-3) / PEAK_HBM, 4)}
+        layer_ops["note"] = ("KV append, attention, o_proj [4096 x 4096] + layer input | RMSNorm, "
+                             "router, top-2 MoE, residual; the pipeline workload's shapes")
+        ops["af_decode_layer"] = layer_ops
+        del lw, ly, lws
+
         # Tiny decoder layer (B=4, 8/2 heads x 64, SwiGLU 512 -> 1408): cache-resident,
         # so its lines are latencies
         wt = synth.tiny_layer(device=dev)

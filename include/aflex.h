@@ -16,6 +16,8 @@
  *   aflex_moe_ffn           top-k mixture-of-experts SwiGLU FFN (Mixtral-8x7B)
  *   aflex_moe_block         RMSNorm + router + MoE FFN (+ residual)
  *   aflex_af_pipeline_step  M microbatches of A then F on two HIP streams
+ *   aflex_af_layer_step     the same over a whole decode layer (KV append,
+ *                           attention, output projection | MoE block)
  *   aflex_kv_append         the new token's K/V into the paged cache
  *   aflex_kv_write          a packed prompt's (or chunk's) K/V into the cache
  *   aflex_linear            y = x W^T (the attention output projection)
@@ -195,6 +197,44 @@ aflex_status aflex_af_pipeline_step(const aflex_attn_args *attn, const aflex_ffn
                                     int32_t M, const int32_t *mb_sizes, int32_t L,
                                     void *workspace, size_t workspace_bytes,
                                     aflex_stream stream_a, aflex_stream stream_f);
+
+/* ------------------------------------------------------------------------ */
+/* The whole decode layer on the interleaved A/F step (section 4.3: the       */
+/* attention group runs attention and sends its output to the FFN group,    */
+/* which runs the FFN block; Eq. 2 times the two stages). For microbatch i:  */
+/*   stream_a: append the new token's K/V (aflex_kv_append), attention,     */
+/*             h_i = x_i + attn_i W_o^T     (x_i: the layer input rows of i, */
+/*                                           or nothing when x_in is NULL)  */
+/*   stream_f: y_i = h_i + MoE(RMSNorm(h_i), RMSNorm(h_i) W_r^T)            */
+/*             (aflex_moe_block with the residual)                           */
+/* h_i [n_i, H] bf16 is the tensor that crosses the A/F boundary. For L > 1 */
+/* step l + 1 of microbatch i takes q = y_i viewed [n_i, Hq, D] and x = y_i  */
+/* (so H must equal Hq * D), appends the same K/V again (the same slot, the */
+/* same values) and starts once F of step l for i is done. attn->out is     */
+/* unused; moe->x and moe->router_logits are unused (may be NULL); moe->y   */
+/* [B, H] receives the last step's output; moe->E >= 1 (the MoE block).     */
+/* ------------------------------------------------------------------------ */
+typedef struct aflex_layer_args {
+  const aflex_bf16 *k_new;          /* [B, Hkv, D] new token's key per sequence */
+  const aflex_bf16 *v_new;          /* [B, Hkv, D] new token's value */
+  aflex_bf16 *k_cache;              /* the pools attn->k_cache / attn->v_cache point at */
+  aflex_bf16 *v_cache;              /*   (written by the append; must be the same pointers) */
+  const aflex_bf16 *w_o;            /* [H, Hq * D] output projection */
+  const aflex_bf16 *x_in;           /* [B, H] layer input added to the projection, or NULL */
+  const aflex_bf16 *norm_weight;    /* [H] RMSNorm gain of the MoE block */
+  const aflex_bf16 *router_weight;  /* [E, H] */
+  float eps;                        /* RMSNorm epsilon (>= 0) */
+} aflex_layer_args;
+
+/* Supported: as aflex_attn_decode, aflex_linear, aflex_moe_block and        */
+/* aflex_af_pipeline_step; H <= 16384. Errors as those entry points.         */
+aflex_status aflex_af_layer_workspace(const aflex_attn_args *attn, const aflex_ffn_args *moe,
+                                      const aflex_layer_args *layer, int32_t M, const int32_t *mb_sizes,
+                                      int32_t L, size_t *bytes);
+aflex_status aflex_af_layer_step(const aflex_attn_args *attn, const aflex_ffn_args *moe,
+                                 const aflex_layer_args *layer, int32_t M, const int32_t *mb_sizes, int32_t L,
+                                 void *workspace, size_t workspace_bytes, aflex_stream stream_a,
+                                 aflex_stream stream_f);
 
 /* ------------------------------------------------------------------------ */
 /* Steps either side of decode attention in the attention stage.            */

@@ -25,6 +25,6 @@ here is "parity unpinned".
 from .attention import attention_decode, attention_weights, gather_sequence  # noqa: F401
 from .ffn import silu, swiglu_ffn  # noqa: F401
 from .moe import route_topk, routing_tables, moe_ffn  # noqa: F401
-from .pipeline import af_layer_steps  # noqa: F401
+from .pipeline import af_decode_layer_steps, af_layer_steps  # noqa: F401
 from .block import kv_append, kv_write, linear, moe_block, rmsnorm  # noqa: F401
 from .prefill import attention_prefill  # noqa: F401

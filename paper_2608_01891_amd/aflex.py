@@ -69,6 +69,11 @@ class PrefillArgs(ctypes.Structure):
                 ("max_seqlen", _i), ("scale", ctypes.c_float)]
 
 
+class LayerArgs(ctypes.Structure):
+    _fields_ = [("k_new", _p), ("v_new", _p), ("k_cache", _p), ("v_cache", _p), ("w_o", _p),
+                ("x_in", _p), ("norm_weight", _p), ("router_weight", _p), ("eps", ctypes.c_float)]
+
+
 class AflexError(RuntimeError):
     def __init__(self, status: int, message: str):
         super().__init__(f"aflex status {status}: {message}")
@@ -106,6 +111,8 @@ def load():
         "aflex_moe_ffn": [FP, _p, ctypes.c_size_t, _p],
         "aflex_af_pipeline_workspace": [AP, FP, _i, I32P, _i, _SZ],
         "aflex_af_pipeline_step": [AP, FP, _i, I32P, _i, _p, ctypes.c_size_t, _p, _p],
+        "aflex_af_layer_workspace": [AP, FP, ctypes.POINTER(LayerArgs), _i, I32P, _i, _SZ],
+        "aflex_af_layer_step": [AP, FP, ctypes.POINTER(LayerArgs), _i, I32P, _i, _p, ctypes.c_size_t, _p, _p],
         "aflex_kv_append": [ctypes.POINTER(KvAppendArgs), _p],
         "aflex_moe_block_workspace": [ctypes.POINTER(MoeBlockArgs), _SZ],
         "aflex_moe_block": [ctypes.POINTER(MoeBlockArgs), _p, ctypes.c_size_t, _p],
@@ -450,6 +457,40 @@ def af_pipeline_step(a, w, logits, k: int, mb_sizes, L: int = 1, y=None, stream_
     p, sz = _ws("pipe", n.value, a.q.device, ws, (stream_a, stream_f))
     _check(lib.aflex_af_pipeline_step(ctypes.byref(aa), ctypes.byref(fa), M, mb, L, p, sz,
                                       _stream(stream_a), _stream(stream_f)))
+    if join:
+        torch.cuda.current_stream(a.q.device).wait_stream(stream_f)
+    return y
+
+
+def af_layer_step(a, w, layer, k: int, mb_sizes, L: int = 1, y=None, stream_a=None, stream_f=None,
+                  ws=None, join: bool = True):
+    """The whole decode layer on the interleaved A/F step: per microbatch KV
+    append, attention and output projection (+ layer input) on stream_a, the
+    MoE block (RMSNorm, router, experts, residual) on stream_f. Appends the
+    new K/V into a's pools in place; returns y [B, H]. Streams as for
+    af_pipeline_step."""
+    lib = load()
+    if stream_a is None or stream_f is None:
+        stream_a, stream_f = pipeline_streams(a.q.device)
+        cur = torch.cuda.current_stream(a.q.device)
+        stream_a.wait_stream(cur)
+        stream_f.wait_stream(cur)
+    if y is None:
+        y = torch.empty(a.B, w.H, dtype=torch.bfloat16, device=a.q.device)
+    aa = attn_args(a, None)
+    fa = ffn_args(None, w, y, None, k)
+    la = LayerArgs(k_new=_ptr(layer.k_new), v_new=_ptr(layer.v_new), k_cache=_ptr(a.k_cache),
+                   v_cache=_ptr(a.v_cache), w_o=_ptr(layer.w_o), x_in=_ptr(layer.x_in),
+                   norm_weight=_ptr(layer.norm_weight), router_weight=_ptr(layer.router_weight),
+                   eps=layer.eps)
+    M = len(mb_sizes)
+    mb = (ctypes.c_int32 * M)(*mb_sizes)
+    n = ctypes.c_size_t()
+    _check(lib.aflex_af_layer_workspace(ctypes.byref(aa), ctypes.byref(fa), ctypes.byref(la), M, mb, L,
+                                        ctypes.byref(n)))
+    p, sz = _ws("layer", n.value, a.q.device, ws, (stream_a, stream_f))
+    _check(lib.aflex_af_layer_step(ctypes.byref(aa), ctypes.byref(fa), ctypes.byref(la), M, mb, L, p, sz,
+                                   _stream(stream_a), _stream(stream_f)))
     if join:
         torch.cuda.current_stream(a.q.device).wait_stream(stream_f)
     return y

@@ -174,6 +174,115 @@ struct EventPool {
 };
 EventPool g_events;
 
+// At least `need` events of the current device for ordering the two streams
+// of a step (created on first use, kept for later calls). The caller holds
+// g_events.mu for as long as it records and waits on them.
+aflex_status pipeline_events(size_t need, std::vector<hipEvent_t>** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_status(e, "pipeline");
+  if ((int)g_events.per_device.size() <= dev) g_events.per_device.resize(dev + 1);
+  std::vector<hipEvent_t>& ev = g_events.per_device[dev];
+  while (ev.size() < need) {
+    hipEvent_t x;
+    e = hipEventCreateWithFlags(&x, hipEventDisableTiming);
+    if (e != hipSuccess) return hip_status(e, "pipeline: event create");
+    ev.push_back(x);
+  }
+  *out = &ev;
+  return AFLEX_OK;
+}
+
+// ---------------------------------------------------------------------------
+// Whole decode layer on the two streams.
+struct LayerLayout {
+  size_t attn_out, h, attn_ws, lin_ws, blk_ws, total;
+};
+
+aflex_linear_args mb_linear(const aflex_attn_args& a, const aflex_ffn_args& f, const aflex_layer_args& ly,
+                            const uint16_t* x, uint16_t* y, int n) {
+  aflex_linear_args l;
+  l.x = x;
+  l.w = ly.w_o;
+  l.y = y;
+  l.T = n;
+  l.K = a.Hq * a.D;
+  l.N = f.H;
+  return l;
+}
+
+aflex_moe_block_args mb_block(const aflex_ffn_args& f, const aflex_layer_args& ly, int off, int n,
+                              const uint16_t* h) {
+  aflex_moe_block_args m;
+  m.ffn = mb_ffn(f, off, n);
+  m.ffn.x = h;
+  m.ffn.router_logits = nullptr;
+  m.norm_weight = ly.norm_weight;
+  m.router_weight = ly.router_weight;
+  m.eps = ly.eps;
+  m.residual = 1;
+  m.router_logits_out = nullptr;
+  return m;
+}
+
+LayerLayout layer_layout(const aflex_attn_args& a, const aflex_ffn_args& f, const aflex_layer_args& ly, int M,
+                         const int32_t* mb) {
+  LayerLayout L;
+  size_t aw = 0, lw = 0, bw = 0;
+  int off = 0;
+  for (int i = 0; i < M; ++i) {
+    const size_t x = aflex::attn_workspace_bytes(mb_attn(a, off, mb[i]));
+    const size_t y = aflex::linear_workspace_bytes(mb_linear(a, f, ly, nullptr, nullptr, mb[i]));
+    const size_t z = aflex::moe_block_workspace_bytes(mb_block(f, ly, off, mb[i], nullptr));
+    aw = x > aw ? x : aw;
+    lw = y > lw ? y : lw;
+    bw = z > bw ? z : bw;
+    off += mb[i];
+  }
+  L.attn_out = 0;
+  L.h = aflex::align_up((size_t)a.B * a.Hq * a.D * 2, 256);
+  L.attn_ws = L.h + aflex::align_up((size_t)a.B * f.H * 2, 256);
+  L.lin_ws = L.attn_ws + aflex::align_up(aw, 256);
+  L.blk_ws = L.lin_ws + aflex::align_up(lw, 256);
+  L.total = L.blk_ws + aflex::align_up(bw, 256);
+  return L;
+}
+
+aflex_status check_layer(const aflex_attn_args* a, const aflex_ffn_args* f, const aflex_layer_args* ly, int32_t M,
+                         const int32_t* mb, int32_t L) {
+  aflex_status s = check_attn(a, false);
+  if (s != AFLEX_OK) return s;
+  REQUIRE(f, AFLEX_ERR_INVALID_ARG, "layer: ffn args is NULL");
+  REQUIRE(ly, AFLEX_ERR_INVALID_ARG, "layer: layer args is NULL");
+  REQUIRE(f->E >= 1, AFLEX_ERR_UNSUPPORTED, "layer: the decode layer step runs the MoE block (E >= 1)");
+  aflex_ffn_args fc = *f;
+  fc.router_logits = reinterpret_cast<const float*>(ly->router_weight);  // computed: only non-NULL matters
+  s = check_ffn(&fc, true, false);
+  if (s != AFLEX_OK) return s;
+  REQUIRE(ly->k_new && ly->v_new && ly->k_cache && ly->v_cache && ly->w_o && ly->norm_weight && ly->router_weight,
+          AFLEX_ERR_INVALID_ARG, "layer: NULL tensor pointer");
+  REQUIRE(ly->k_cache == a->k_cache && ly->v_cache == a->v_cache, AFLEX_ERR_INVALID_ARG,
+          "layer: k_cache / v_cache must be the pools the attention reads");
+  REQUIRE(isfinite(ly->eps) && ly->eps >= 0.f, AFLEX_ERR_INVALID_ARG, "layer: eps must be finite and >= 0");
+  REQUIRE(f->H <= 16384, AFLEX_ERR_UNSUPPORTED, "layer: H=%d above 16384", f->H);
+  REQUIRE(aligned16(ly->k_new) && aligned16(ly->v_new) && aligned16(ly->w_o) && aligned16(ly->norm_weight) &&
+              aligned16(ly->router_weight) && (!ly->x_in || aligned16(ly->x_in)),
+          AFLEX_ERR_ALIGNMENT, "layer: tensors must be 16-byte aligned");
+  REQUIRE(M >= 1 && M <= 64, AFLEX_ERR_INVALID_ARG, "layer: M=%d must be in [1, 64]", M);
+  REQUIRE(mb, AFLEX_ERR_INVALID_ARG, "layer: mb_sizes is NULL");
+  REQUIRE(L >= 1, AFLEX_ERR_INVALID_ARG, "layer: L=%d must be >= 1", L);
+  long long sum = 0;
+  for (int i = 0; i < M; ++i) {
+    REQUIRE(mb[i] >= 1, AFLEX_ERR_INVALID_ARG, "layer: mb_sizes[%d]=%d must be >= 1", i, mb[i]);
+    sum += mb[i];
+  }
+  REQUIRE(sum == a->B, AFLEX_ERR_INVALID_ARG, "layer: sum of mb_sizes %lld != B %d", sum, a->B);
+  REQUIRE(f->T == a->B, AFLEX_ERR_INVALID_ARG, "layer: ffn T %d != attention B %d", f->T, a->B);
+  REQUIRE(L == 1 || f->H == a->Hq * a->D, AFLEX_ERR_INVALID_ARG,
+          "layer: L > 1 feeds y back as q, so H (%d) must equal Hq*D (%d)", f->H, a->Hq * a->D);
+  return AFLEX_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -440,19 +549,12 @@ aflex_status aflex_af_pipeline_step(const aflex_attn_args* a, const aflex_ffn_ar
   void* ffn_ws = w + P.ffn_ws;
   const int H = f->H;
 
-  int dev = 0;
-  hipError_t e = hipGetDevice(&dev);
-  if (e != hipSuccess) return hip_status(e, "pipeline");
+  hipError_t e;
   std::lock_guard<std::mutex> lock(g_events.mu);
-  if ((int)g_events.per_device.size() <= dev) g_events.per_device.resize(dev + 1);
-  std::vector<hipEvent_t>& ev = g_events.per_device[dev];
-  const size_t need = 2 * (size_t)M + 1;
-  while (ev.size() < need) {
-    hipEvent_t x;
-    e = hipEventCreateWithFlags(&x, hipEventDisableTiming);
-    if (e != hipSuccess) return hip_status(e, "pipeline: event create");
-    ev.push_back(x);
-  }
+  std::vector<hipEvent_t>* evp = nullptr;
+  s = pipeline_events(2 * (size_t)M + 1, &evp);
+  if (s != AFLEX_OK) return s;
+  std::vector<hipEvent_t>& ev = *evp;
   hipEvent_t entry = ev[0];
   hipEvent_t* evA = &ev[1];
   hipEvent_t* evF = &ev[1 + M];
@@ -495,6 +597,87 @@ aflex_status aflex_af_pipeline_step(const aflex_attn_args* a, const aflex_ffn_ar
                : aflex::launch_swiglu(fm, ffn_ws, sf);
       if (e != hipSuccess) return hip_status(e, "pipeline: ffn");
       if ((e = hipEventRecord(evF[i], sf)) != hipSuccess) return hip_status(e, "pipeline");
+      off += n;
+    }
+  }
+  return AFLEX_OK;
+}
+
+aflex_status aflex_af_layer_workspace(const aflex_attn_args* a, const aflex_ffn_args* f, const aflex_layer_args* ly,
+                                      int32_t M, const int32_t* mb, int32_t L, size_t* bytes) {
+  REQUIRE(bytes, AFLEX_ERR_INVALID_ARG, "layer: bytes is NULL");
+  aflex_status s = check_layer(a, f, ly, M, mb, L);
+  if (s != AFLEX_OK) return s;
+  *bytes = layer_layout(*a, *f, *ly, M, mb).total;
+  return AFLEX_OK;
+}
+
+aflex_status aflex_af_layer_step(const aflex_attn_args* a, const aflex_ffn_args* f, const aflex_layer_args* ly,
+                                 int32_t M, const int32_t* mb, int32_t L, void* ws, size_t ws_bytes,
+                                 aflex_stream stream_a, aflex_stream stream_f) {
+  aflex_status s = check_layer(a, f, ly, M, mb, L);
+  if (s != AFLEX_OK) return s;
+  const LayerLayout P = layer_layout(*a, *f, *ly, M, mb);
+  s = check_ws(ws, ws_bytes, P.total, "layer");
+  if (s != AFLEX_OK) return s;
+  REQUIRE(stream_a != stream_f, AFLEX_ERR_INVALID_ARG, "layer: stream_a and stream_f must differ");
+
+  hipStream_t sa = (hipStream_t)stream_a, sf = (hipStream_t)stream_f;
+  char* w = static_cast<char*>(ws);
+  uint16_t* attn_out = reinterpret_cast<uint16_t*>(w + P.attn_out);
+  uint16_t* h = reinterpret_cast<uint16_t*>(w + P.h);
+  const int H = f->H, HqD = a->Hq * a->D, kvrow = a->Hkv * a->D;
+
+  hipError_t e;
+  std::lock_guard<std::mutex> lock(g_events.mu);
+  std::vector<hipEvent_t>* evp = nullptr;
+  s = pipeline_events(2 * (size_t)M + 1, &evp);
+  if (s != AFLEX_OK) return s;
+  std::vector<hipEvent_t>& ev = *evp;
+  hipEvent_t entry = ev[0];
+  hipEvent_t* evA = &ev[1];
+  hipEvent_t* evF = &ev[1 + M];
+
+  // Work still queued on stream_f from an earlier call may read the buffers
+  // the first attention stage overwrites.
+  if ((e = hipEventRecord(entry, sf)) != hipSuccess) return hip_status(e, "layer");
+  if ((e = hipStreamWaitEvent(sa, entry, 0)) != hipSuccess) return hip_status(e, "layer");
+
+  for (int l = 0; l < L; ++l) {
+    int off = 0;
+    for (int i = 0; i < M; ++i) {
+      const int n = mb[i];
+      if (l > 0 && (e = hipStreamWaitEvent(sa, evF[i], 0)) != hipSuccess) return hip_status(e, "layer");
+      // attention stage: append, attention, projection (+ the layer input)
+      aflex_kv_append_args ka;
+      ka.k_new = ly->k_new + (size_t)off * kvrow;
+      ka.v_new = ly->v_new + (size_t)off * kvrow;
+      ka.k_cache = ly->k_cache;
+      ka.v_cache = ly->v_cache;
+      ka.block_table = a->block_table + (size_t)off * a->max_blocks_per_seq;
+      ka.context_lens = a->context_lens + off;
+      ka.B = n;
+      ka.Hkv = a->Hkv;
+      ka.D = a->D;
+      ka.block_size = a->block_size;
+      ka.max_blocks_per_seq = a->max_blocks_per_seq;
+      ka.num_blocks = a->num_blocks;
+      if ((e = aflex::launch_kv_append(ka, sa)) != hipSuccess) return hip_status(e, "layer: kv append");
+      aflex_attn_args am = mb_attn(*a, off, n);
+      if (l > 0) am.q = f->y + (size_t)off * H;
+      am.out = attn_out + (size_t)off * HqD;
+      const bool alone = l == 0 && i == 0;  // before any FFN work, as in aflex_af_pipeline_step
+      if ((e = aflex::launch_attn_decode(am, w + P.attn_ws, sa, alone)) != hipSuccess)
+        return hip_status(e, "layer: attn");
+      const uint16_t* res = l > 0 ? f->y + (size_t)off * H : (ly->x_in ? ly->x_in + (size_t)off * H : nullptr);
+      const aflex_linear_args lin = mb_linear(*a, *f, *ly, am.out, h + (size_t)off * H, n);
+      if ((e = aflex::launch_linear(lin, w + P.lin_ws, sa, res)) != hipSuccess) return hip_status(e, "layer: o_proj");
+      if ((e = hipEventRecord(evA[i], sa)) != hipSuccess) return hip_status(e, "layer");
+      // FFN stage: the MoE block on the hidden state that crossed the boundary
+      if ((e = hipStreamWaitEvent(sf, evA[i], 0)) != hipSuccess) return hip_status(e, "layer");
+      const aflex_moe_block_args blk = mb_block(*f, *ly, off, n, h + (size_t)off * H);
+      if ((e = aflex::launch_moe_block(blk, w + P.blk_ws, sf)) != hipSuccess) return hip_status(e, "layer: moe block");
+      if ((e = hipEventRecord(evF[i], sf)) != hipSuccess) return hip_status(e, "layer");
       off += n;
     }
   }

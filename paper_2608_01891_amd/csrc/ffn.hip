@@ -18,11 +18,19 @@ namespace aflex {
 
 __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restrict__ P, long long split_stride,
                                                             int splits, long long n4,
-                                                            uint16_t* __restrict__ y) {
+                                                            uint16_t* __restrict__ y,
+                                                            const uint16_t* __restrict__ residual) {
   const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
   if (i >= n4) return;
   f32x4 s = *reinterpret_cast<const f32x4*>(P + i * 4);
   for (int k = 1; k < splits; ++k) s += *reinterpret_cast<const f32x4*>(P + k * split_stride + i * 4);
+  if (residual) {  // added after the split sum, before the one rounding
+    const ushort4 r = *reinterpret_cast<const ushort4*>(residual + i * 4);
+    s[0] += bf2f(r.x);
+    s[1] += bf2f(r.y);
+    s[2] += bf2f(r.z);
+    s[3] += bf2f(r.w);
+  }
   ushort4 o;
   o.x = f2bf(s[0]);
   o.y = f2bf(s[1]);
@@ -86,18 +94,19 @@ hipError_t launch_swiglu(const aflex_ffn_args& f, void* ws, hipStream_t stream) 
   const long long n4 = (long long)f.T * f.H / 4;
   ProfScope ps("splitk_reduce", stream);
   splitk_reduce_kernel<<<(unsigned)((n4 + 255) / 256), 256, 0, stream>>>(P, d.p_split_stride, pl.down_splits, n4,
-                                                                       f.y);
+                                                                       f.y, nullptr);
   return hipGetLastError();
 }
 
-// Linear layer y = x W^T: the down-GEMM tiles with split-K and the same
-// fixed-order reduction (bf16 out directly when a single split suffices).
+// Linear layer y = x W^T (+ residual): the down-GEMM tiles with split-K and
+// the same fixed-order reduction (bf16 out directly when a single split
+// suffices); the optional residual is added before the one rounding.
 size_t linear_workspace_bytes(const aflex_linear_args& l) {
   const FfnPlan pl = plan_dense(l.T, l.N, l.K);
   return pl.down_splits > 1 ? align_up((size_t)pl.down_splits * l.T * l.N * 4, 256) : 256;
 }
 
-hipError_t launch_linear(const aflex_linear_args& l, void* ws, hipStream_t stream) {
+hipError_t launch_linear(const aflex_linear_args& l, void* ws, hipStream_t stream, const uint16_t* residual) {
   const FfnPlan pl = plan_dense(l.T, l.N, l.K);
   float* P = static_cast<float*>(ws);
   GemmParams d = {};
@@ -118,12 +127,13 @@ hipError_t launch_linear(const aflex_linear_args& l, void* ws, hipStream_t strea
   d.P = P;
   d.p_split_stride = (long long)l.T * l.N;
   d.ldp = l.N;
+  d.R = residual;
   hipError_t e = launch_down(pl.bm, pl.down_splits > 1, l.T <= pl.bm, d, stream);
   if (e != hipSuccess || pl.down_splits == 1) return e;
   const long long n4 = (long long)l.T * l.N / 4;
   ProfScope ps("splitk_reduce", stream);
   splitk_reduce_kernel<<<(unsigned)((n4 + 255) / 256), 256, 0, stream>>>(P, d.p_split_stride, pl.down_splits, n4,
-                                                                       l.y);
+                                                                       l.y, residual);
   return hipGetLastError();
 }
 

@@ -18,7 +18,7 @@
 //           applies SiLU(gate) * up and stores bf16 (the fused SwiGLU step).
 //   OUT_F32 store the fp32 accumulator into split-K partials (one slice per
 //           split; a later kernel sums the slices in a fixed order).
-//   neither store bf16.
+//   neither store bf16 (plus an optional bf16 residual, one rounding).
 //
 // Work decomposition: a 1-D grid over (m-tile, n-tile, k-split). Work-groups
 // are dispatched round-robin over the 8 XCDs; the logical tile index is
@@ -54,6 +54,7 @@ struct GemmParams {
   int mt_major;               // 1: m-tile is the slow index of the tile order
   uint16_t* C;                // bf16 output [rows, ldc]
   int ldc;
+  const uint16_t* R;          // optional bf16 residual [rows, ldc] added before rounding (plain bf16 output only)
   float* P;                   // fp32 split-K partials [splits][rows][ldp]
   long long p_split_stride;
   int ldp;
@@ -369,7 +370,8 @@ __global__ __launch_bounds__(64 * WM * WN, LDS_BYTES > 81920 ? 1 : 2) void gemm_
           const float h = g / (1.f + __expf(-g)) * u;
           p.C[(size_t)row * p.ldc + col] = f2bf(h);
         } else {
-          p.C[(size_t)row * p.ldc + col] = f2bf(acc[0][i][j][e]);
+          const float r = p.R ? bf2f(p.R[(size_t)row * p.ldc + col]) : 0.f;
+          p.C[(size_t)row * p.ldc + col] = f2bf(acc[0][i][j][e] + r);
         }
       }
     }

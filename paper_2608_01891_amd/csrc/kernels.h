@@ -34,7 +34,8 @@ hipError_t launch_swiglu(const aflex_ffn_args& f, void* ws, hipStream_t stream);
 hipError_t launch_kv_append(const aflex_kv_append_args& a, hipStream_t stream);
 hipError_t launch_kv_write(const aflex_kv_write_args& a, hipStream_t stream);
 size_t linear_workspace_bytes(const aflex_linear_args& l);
-hipError_t launch_linear(const aflex_linear_args& l, void* ws, hipStream_t stream);
+hipError_t launch_linear(const aflex_linear_args& l, void* ws, hipStream_t stream,
+                         const uint16_t* residual = nullptr);
 
 // Top-k MoE FFN (moe.hip).
 size_t moe_workspace_bytes(const aflex_ffn_args& f);

@@ -119,7 +119,8 @@ def normal_tensor(seed: int, stream: int, shape, scale: float = 1.0,
 
 # stream ids of the bulk tensors
 STREAM = {"q": 1, "k": 2, "v": 3, "x": 4, "w_gate": 5, "w_up": 6, "w_down": 7,
-          "prefill_q": 8, "prefill_k": 9, "prefill_v": 10}
+          "prefill_q": 8, "prefill_k": 9, "prefill_v": 10,
+          "k_new": 11, "v_new": 12, "w_o": 13, "x_in": 14, "norm": 15, "w_router": 16}
 WEIGHT_SIGMA = 0.02
 BLOCK_SIZE = 16
 
@@ -334,6 +335,41 @@ def prefill_workload(model: str = "qwen3-32b", prompt_len: int = 4096, prompts: 
 def prefill_ffn_tokens(H: int, T: int, device="cpu") -> torch.Tensor:
     """FFN input [T, H] of a prefill batch (all prompt tokens at once)."""
     return normal_tensor(7, STREAM["x"], (T, H), device=device)
+
+
+@dataclass
+class LayerInputs:
+    """The rest of a decode layer around the A/F operator pair: the new token's
+    K/V per sequence, the output projection, the layer input (residual) and the
+    MoE block's RMSNorm gain and router."""
+    k_new: torch.Tensor          # [B, Hkv, D] bf16
+    v_new: torch.Tensor          # [B, Hkv, D] bf16
+    w_o: torch.Tensor            # [H, Hq * D] bf16
+    x_in: torch.Tensor | None    # [B, H] bf16 (None: no residual on the projection)
+    norm_weight: torch.Tensor    # [H] bf16
+    router_weight: torch.Tensor  # [E, H] bf16
+    eps: float = 1e-5
+
+    def to(self, device):
+        d = dict(self.__dict__)
+        for k in ("k_new", "v_new", "w_o", "x_in", "norm_weight", "router_weight"):
+            if d[k] is not None:
+                d[k] = d[k].to(device)
+        return LayerInputs(**d)
+
+
+def make_layer(seed: int, B: int, Hq: int, Hkv: int, D: int, H: int, E: int, residual: bool = True,
+               device="cpu") -> LayerInputs:
+    """Decode-layer inputs: K/V and x ~ N(0,1), W_o and W_r ~ N(0, 0.02),
+    RMSNorm gain 1 + 0.1 N(0,1) (all bf16)."""
+    kn = normal_tensor(seed, STREAM["k_new"], (B, Hkv, D), device=device)
+    vn = normal_tensor(seed, STREAM["v_new"], (B, Hkv, D), device=device)
+    wo = normal_tensor(seed, STREAM["w_o"], (H, Hq * D), WEIGHT_SIGMA, device)
+    x = normal_tensor(seed, STREAM["x_in"], (B, H), device=device) if residual else None
+    g = (1.0 + 0.1 * normal_tensor(seed, STREAM["norm"], (H,), dtype=torch.float32, device=device)
+         ).to(torch.bfloat16)
+    wr = normal_tensor(seed, STREAM["w_router"], (E, H), WEIGHT_SIGMA, device)
+    return LayerInputs(k_new=kn, v_new=vn, w_o=wo, x_in=x, norm_weight=g, router_weight=wr)
 
 
 def custom_attention(seed: int, B: int, Hq: int, Hkv: int, D: int, ctx, ctx_hi: int | None = None,

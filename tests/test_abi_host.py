@@ -21,7 +21,7 @@ def lib():
 
 def test_exports_every_declared_symbol(lib):
     names = aflex.exported_names()
-    assert len(names) == 23
+    assert len(names) == 25
     for n in names:
         assert hasattr(lib, n), n
     assert lib.aflex_version().startswith(b"aflex")
@@ -207,3 +207,42 @@ def test_pool_streams_validation(lib):
     sf = ctypes.c_void_p()
     assert lib.aflex_pool_streams_create(100, ctypes.byref(sa), ctypes.byref(sf)) == aflex.ERR_UNSUPPORTED
     assert sa.value is None and sf.value is None
+
+
+def _layer_status(lib, a, f, la, M=2, mbs=(2, 2), L=1):
+    mb = (ctypes.c_int32 * M)(*mbs)
+    n = ctypes.c_size_t()
+    return lib.aflex_af_layer_workspace(ctypes.byref(a), ctypes.byref(f), ctypes.byref(la), M, mb, L,
+                                        ctypes.byref(n))
+
+
+@pytest.mark.parametrize("case,status", [
+    ("ok", aflex.OK),
+    ("dense", aflex.ERR_UNSUPPORTED),
+    ("other_pool", aflex.ERR_INVALID_ARG),
+    ("no_router", aflex.ERR_INVALID_ARG),
+    ("misaligned_wo", aflex.ERR_ALIGNMENT),
+    ("L2_hidden_mismatch", aflex.ERR_INVALID_ARG),
+    ("bad_eps", aflex.ERR_INVALID_ARG),
+])
+def test_layer_step_validation(lib, case, status):
+    """The decode-layer step validates on the host: the MoE block only (E >= 1),
+    the append must target the pools the attention reads, L > 1 needs H = Hq*D."""
+    a = _attn(out=None)                       # B=4, Hq=8, Hkv=2, D=64: Hq*D = 512
+    f = _ffn(x=None, router_logits=None, H=512, I=1408, E=8, k=2)
+    la = aflex.LayerArgs(k_new=FAKE, v_new=FAKE, k_cache=FAKE, v_cache=FAKE, w_o=FAKE, x_in=None,
+                         norm_weight=FAKE, router_weight=FAKE, eps=1e-5)
+    L = 1
+    if case == "dense":
+        f.E, f.k = 0, 0
+    elif case == "other_pool":
+        la.k_cache = FAKE + 256
+    elif case == "no_router":
+        la.router_weight = None
+    elif case == "misaligned_wo":
+        la.w_o = FAKE + 2
+    elif case == "L2_hidden_mismatch":
+        f.H, L = 1024, 2
+    elif case == "bad_eps":
+        la.eps = -1.0
+    assert _layer_status(lib, a, f, la, L=L) == status
