@@ -333,14 +333,17 @@ __global__ __launch_bounds__(64 * WM * WN, LDS_BYTES > 81920 ? 1 : 2) void gemm_
     using I1 = std::integral_constant<int, 1>;
     using I2 = std::integral_constant<int, 2 <= TM ? 2 : TM>;
     using I3 = std::integral_constant<int, 3 <= TM ? 3 : TM>;
+    using I4 = std::integral_constant<int, 4 <= TM ? 4 : TM>;
     using IT = std::integral_constant<int, TM>;
-    static_assert(TM <= 4, "row blocks per wave");
+    static_assert(TM <= 5, "row blocks per wave");
     if (nact == 1)
       kloop(I1{});
     else if (nact == 2)
       kloop(I2{});
     else if (nact == 3)
       kloop(I3{});
+    else if (nact == 4 || TM == 4)
+      kloop(I4{});
     else
       kloop(IT{});
   }

@@ -2,9 +2,10 @@
 //
 // Row-tile size selects the shape: 32- and 64-row tiles stream weights (4
 // waves, 16x16x32 MFMA, 64-wide k-steps, two work-groups per CU, HBM-bound);
-// 128- and 256-row tiles are the 8-wave 32x32x16 MFMA shapes (wave tiles of
-// 64 or 128 rows by 32 columns of each gate/up matrix or 64 columns of the
-// down matrix, one work-group per CU in the whole 160 KiB of LDS). Both take
+// 128-, 256- and 320-row tiles are the 8-wave 32x32x16 MFMA shapes (wave
+// tiles of 64, 128 or 160 rows by 32 columns of each gate/up matrix or 64
+// columns of the down matrix, one work-group per CU in the whole 160 KiB of
+// LDS; the 320-row tiles take 240 registers, still two waves per SIMD). Both take
 // 64-wide k-steps, so every k-step reads whole 128-byte lines of each row: a
 // ring of three stages for the 128-row tiles, two (the next k-step loads
 // while the current one is multiplied) for the 256-row tiles, which was
@@ -48,6 +49,7 @@ hipError_t launch_gate_up(int bm, bool once, const GemmParams& g, hipStream_t st
       else
         go<128, 128, 2, 4, 64, 32, true, false, 163840>(g, grid, stream);
       break;
+    case 320: go<320, 128, 2, 4, 64, 32, true, false, 163840>(g, grid, stream); break;
     default: go<256, 128, 2, 4, 64, 32, true, false, 163840>(g, grid, stream); break;
   }
   return hipGetLastError();
@@ -69,6 +71,7 @@ static void down(int bm, bool once, const GemmParams& g, unsigned grid, hipStrea
       else
         go<128, 256, 2, 4, 64, 32, false, F32, 163840>(g, grid, stream);
       break;
+    case 320: go<320, 256, 2, 4, 64, 32, false, F32, 163840>(g, grid, stream); break;
     default: go<256, 256, 2, 4, 64, 32, false, F32, 163840>(g, grid, stream); break;
   }
 }

@@ -136,12 +136,13 @@ def test_routing_extremes(gpu_lib, T, E, k):
     check_rows(y.cpu(), ref, what=f"moe extremes T={T} E={E} k={k}")
 
 
-@pytest.mark.parametrize("T", [20, 160, 200, 384, 448, 576, 584, 600])
+@pytest.mark.parametrize("T", [20, 160, 200, 384, 448, 576, 584, 600, 1024, 1200, 2048, 2500])
 def test_tile_shape_boundaries(gpu_lib, T):
     """Average rows per expert on both sides of the tile-size thresholds with 8
     experts and top-2: 32-row tiles (5), 64-row (40), 128-row with
-    non-temporal weights (50, 96), 128-row re-reading weights (112, 144) and
-    256-row tiles (146, 150)."""
+    non-temporal weights (50, 96), 128-row re-reading weights (112, 144),
+    256-row tiles (146, 150, 300, 625) and 320-row tiles (256, 512; experts
+    of either side of 320 and 640 rows)."""
     x, w, logits = synth.custom_ffn(90 + T, T, 256, 192, E=8)
     y = aflex.moe_ffn(x.to(DEV), w.to(DEV), logits.to(DEV), 2).cpu()
     ref, _, _ = oracle.moe_ffn(x, logits, w.w_gate, w.w_up, w.w_down, 2)
