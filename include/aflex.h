@@ -317,7 +317,10 @@ typedef struct aflex_prefill_args {
   const int32_t *cu_seqlens;    /* [B+1] device, 0 = cu[0] <= cu[1] <= ... <= cu[B] = T */
   aflex_bf16 *out;              /* [T, Hq, D] */
   int32_t B, T, Hq, Hkv, D;
-  int32_t max_seqlen;           /* host-known bound on every prompt length; sizes the grid */
+  int32_t max_seqlen;           /* host-known bound on every prompt length; sizes the grid and
+                                   selects the work-group shape (two query heads per
+                                   work-group from 2048 on, for an even Hq / Hkv), so a
+                                   tight bound keeps short prompts on the faster shape */
   float scale;                  /* softmax scale; 0 selects 1/sqrt(D) */
 } aflex_prefill_args;
 
