@@ -46,7 +46,8 @@ def _check(y, lg, r, ref_y, ref_lg, ref_ids, k, rows=None):
 
 
 @pytest.mark.parametrize("T,H,I,E,k,res", [(37, 128, 192, 6, 3, False), (64, 256, 128, 8, 2, True),
-                                           (5, 512, 256, 4, 1, True)])
+                                           (5, 512, 256, 4, 1, True), (9, 2048, 128, 16, 2, False),
+                                           (3, 8192, 128, 8, 2, True), (2, 16384, 64, 20, 4, False)])
 def test_small_shapes(gpu_lib, T, H, I, E, k, res):
     x, w, gamma, wr = _inputs(120 + T, T, H, I, E)
     y, lg, r = aflex.moe_block(x.to(DEV), w.to(DEV), gamma.to(DEV), wr.to(DEV), k, eps=1e-5,
