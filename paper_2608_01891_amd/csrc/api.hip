@@ -444,7 +444,7 @@ aflex_status aflex_attn_decode(const aflex_attn_args* a, void* ws, size_t ws_byt
   if (s != AFLEX_OK) return s;
   s = check_ws(ws, ws_bytes, aflex::attn_workspace_bytes(*a), "attn");
   if (s != AFLEX_OK) return s;
-  return hip_status(aflex::launch_attn_decode(*a, ws, (hipStream_t)stream, true), "attn");
+  return hip_status(aflex::launch_attn_decode(*a, ws, (hipStream_t)stream), "attn");
 }
 
 aflex_status aflex_attn_decode_noalloc(const aflex_attn_args* a, aflex_stream stream) {
@@ -458,7 +458,7 @@ aflex_status aflex_attn_decode_noalloc(const aflex_attn_args* a, aflex_stream st
   void* ws = nullptr;
   hipError_t e = aflex::static_scratch(&ws);
   if (e != hipSuccess) return hip_status(e, "attn_noalloc: static scratch");
-  return hip_status(aflex::launch_attn_decode(*a, ws, (hipStream_t)stream, true), "attn_noalloc");
+  return hip_status(aflex::launch_attn_decode(*a, ws, (hipStream_t)stream), "attn_noalloc");
 }
 
 aflex_status aflex_ffn_swiglu_workspace(const aflex_ffn_args* f, size_t* bytes) {
@@ -584,11 +584,7 @@ aflex_status aflex_af_pipeline_step(const aflex_attn_args* a, const aflex_ffn_ar
       aflex_attn_args am = mb_attn(*a, off, n);
       if (l > 0) am.q = f->y + (size_t)off * H;
       am.out = attn_out + (size_t)off * H;
-      // The first attention runs before any FFN work (only the routing
-      // overlaps it): non-temporal K/V loads as for attention on its own;
-      // the others share HBM and caches with an FFN weight stream.
-      const bool alone = l == 0 && i == 0;
-      if ((e = aflex::launch_attn_decode(am, attn_ws, sa, alone)) != hipSuccess) return hip_status(e, "pipeline: attn");
+      if ((e = aflex::launch_attn_decode(am, attn_ws, sa)) != hipSuccess) return hip_status(e, "pipeline: attn");
       if ((e = hipEventRecord(evA[i], sa)) != hipSuccess) return hip_status(e, "pipeline");
       if ((e = hipStreamWaitEvent(sf, evA[i], 0)) != hipSuccess) return hip_status(e, "pipeline");
       aflex_ffn_args fm = mb_ffn(*f, off, n);
@@ -666,9 +662,7 @@ aflex_status aflex_af_layer_step(const aflex_attn_args* a, const aflex_ffn_args*
       aflex_attn_args am = mb_attn(*a, off, n);
       if (l > 0) am.q = f->y + (size_t)off * H;
       am.out = attn_out + (size_t)off * HqD;
-      const bool alone = l == 0 && i == 0;  // before any FFN work, as in aflex_af_pipeline_step
-      if ((e = aflex::launch_attn_decode(am, w + P.attn_ws, sa, alone)) != hipSuccess)
-        return hip_status(e, "layer: attn");
+      if ((e = aflex::launch_attn_decode(am, w + P.attn_ws, sa)) != hipSuccess) return hip_status(e, "layer: attn");
       const uint16_t* res = l > 0 ? f->y + (size_t)off * H : (ly->x_in ? ly->x_in + (size_t)off * H : nullptr);
       const aflex_linear_args lin = mb_linear(*a, *f, *ly, am.out, h + (size_t)off * H, n);
       if ((e = aflex::launch_linear(lin, w + P.lin_ws, sa, res)) != hipSuccess) return hip_status(e, "layer: o_proj");

@@ -467,7 +467,7 @@ size_t attn_workspace_bytes(const aflex_attn_args& a) {
          align_up(U * sizeof(int2), 256);
 }
 
-hipError_t launch_attn_decode(const aflex_attn_args& a, void* ws, hipStream_t stream, bool nt_kv) {
+hipError_t launch_attn_decode(const aflex_attn_args& a, void* ws, hipStream_t stream) {
   AttnParams p;
   p.q = a.q;
   p.kc = a.k_cache;
@@ -497,17 +497,10 @@ hipError_t launch_attn_decode(const aflex_attn_args& a, void* ws, hipStream_t st
   p.span = reinterpret_cast<int2*>(w);
   {
     ProfScope ps("attn_decode", stream);
-    if (a.D == 128) {
-      if (nt_kv)
-        attn_decode_kernel<128, true><<<P, 256, 0, stream>>>(p);
-      else
-        attn_decode_kernel<128, false><<<P, 256, 0, stream>>>(p);
-    } else {
-      if (nt_kv)
-        attn_decode_kernel<64, true><<<P, 256, 0, stream>>>(p);
-      else
-        attn_decode_kernel<64, false><<<P, 256, 0, stream>>>(p);
-    }
+    if (a.D == 128)
+      attn_decode_kernel<128, true><<<P, 256, 0, stream>>>(p);
+    else
+      attn_decode_kernel<64, true><<<P, 256, 0, stream>>>(p);
   }
   if (P > 1) {  // with one work-group no unit is split
     ProfScope ps("attn_merge", stream);

@@ -20,11 +20,10 @@ hipError_t static_scratch(void** ptr);
 // range B * Hkv * ceil(max_context_len / 16) stays below 2^30.
 bool attn_shape_fits(const aflex_attn_args& a);
 size_t attn_workspace_bytes(const aflex_attn_args& a);
-// nt_kv: stream the K/V tiles with non-temporal loads. Decode attention on its
-// own (an attention pool) reads each cached byte once and measured 2-4% faster
-// that way; next to the FFN's weight stream on the same GPU (the two-stream
-// pipeline) ordinary loads measured ~1% faster.
-hipError_t launch_attn_decode(const aflex_attn_args& a, void* ws, hipStream_t stream, bool nt_kv);
+// K/V tiles stream with non-temporal loads: every cached byte is read once,
+// alone and next to the FFN's weight stream in the two-stream step alike
+// (that step: 2.785 -> 2.730 ms against ordinary loads).
+hipError_t launch_attn_decode(const aflex_attn_args& a, void* ws, hipStream_t stream);
 
 // Dense SwiGLU FFN (ffn.hip).
 size_t swiglu_workspace_bytes(const aflex_ffn_args& f);
