@@ -63,11 +63,18 @@ struct AttnParams {
   int B, Hq, Hkv, G;
   int max_blocks, num_blocks, max_ctx;
   int chunk_blocks;              // > 0: fixed blocks per work-group; 0: even split over the grid
+  int unit_cost;                 // extra cost of a unit in block positions (0 with fixed pieces)
   float scale_log2;              // softmax scale * log2(e)
 };
 
 constexpr int kWaves = 4;
 constexpr int kMinChunkBlocks = 8;  // one pair per wave at least
+// Charge per (sequence, kv head) unit, in 16-token blocks, when the grid
+// splits the units evenly: a piece costs its work-group about one loaded round
+// trip to memory besides its blocks (the waves drain at its end, the merge
+// through LDS runs, the next piece's first loads start cold), so work-groups
+// covering many short units get fewer blocks.
+constexpr int kUnitCost = 8;
 
 __device__ __forceinline__ int clamp_ctx(const AttnParams& p, int b) {
   int c = p.cl[b];
@@ -114,13 +121,21 @@ __device__ __forceinline__ int load_block_id(const AttnParams& p, int b, int jb,
   return id;
 }
 
-// Partition of the flattened block range, as the decode kernel computes it:
-// per kv head the blocks of all sequences (total) and blocks per work-group.
+// Positions a (sequence, kv head) unit of sequence b takes in the flattened
+// range: its blocks plus a fixed charge for the piece it adds (zero for a
+// sequence with no cached token, which has no unit).
+__device__ __forceinline__ int unit_len(const AttnParams& p, int b) {
+  const int n = nblk_of(clamp_ctx(p, b));
+  return n > 0 ? n + p.unit_cost : 0;
+}
+
+// Partition of the flattened range, as the decode kernel computes it: the
+// total over all units (W) and the positions per work-group.
 __device__ __forceinline__ int chunk_of(const AttnParams& p, int P, int lane, int* W_out) {
   int total = 0;
   for (int c = 0; c < p.B; c += 64) {
     const int b = c + lane;
-    total += wave_sum_i(b < p.B ? nblk_of(clamp_ctx(p, b)) : 0);
+    total += wave_sum_i(b < p.B ? unit_len(p, b) : 0);
   }
   const int W = __builtin_amdgcn_readfirstlane(total) * p.Hkv;
   *W_out = W;
@@ -162,12 +177,15 @@ __global__ __launch_bounds__(256, 3) void attn_decode_kernel(AttnParams p) {
   if (x0 >= W) return;
   const int x1 = min(x0 + C, W);
 
-  // First sequence whose blocks reach past x0: base = its first block position
-  // per kv head (x positions are base * Hkv + kvh * nblk + j).
+  // First sequence whose units reach past x0: base = its first position per
+  // kv head. Unit (b, kvh) spans positions [S, S + len) with
+  // S = base * Hkv + kvh * len and len = nblk + unit_cost; its block j sits at
+  // S + unit_cost + j, so a work-group whose range lies in a unit's leading
+  // charge holds no piece of it.
   int b = 0, base = 0;
   for (int c = 0; c < p.B; c += 64) {
     const int bb = c + lane;
-    const int n = bb < p.B ? nblk_of(clamp_ctx(p, bb)) : 0;
+    const int n = bb < p.B ? unit_len(p, bb) : 0;
     const int incl = wave_incl_scan(n, lane);
     const unsigned long long past = __ballot((base + incl) * Hkv > x0);
     if (past) {
@@ -181,8 +199,9 @@ __global__ __launch_bounds__(256, 3) void attn_decode_kernel(AttnParams p) {
   // (every value that steers the piece loop is wave-uniform: scalar registers)
   b = __builtin_amdgcn_readfirstlane(b);
   base = __builtin_amdgcn_readfirstlane(base);
+  const int uc = p.unit_cost;
   int nb = nblk_of(clamp_ctx(p, b));
-  int kvh = (x0 - base * Hkv) / nb;
+  int kvh = (x0 - base * Hkv) / (nb + uc);
 
   // Token slots. QK tile row rr (lane rr loads it) holds token
   //   block (rr >> 3), offset ((rr >> 2) & 1) * 8 + (rr & 3)    [first product]
@@ -201,28 +220,35 @@ __global__ __launch_bounds__(256, 3) void attn_decode_kernel(AttnParams p) {
   // First block-id chunk of the current piece; each piece loads the next
   // piece's first chunk while it streams, so a new piece starts with its K/V
   // loads instead of a round trip for its block ids.
-  int piece_ids = load_block_id(p, b, x0 - (base * Hkv + kvh * nb) + lane, min(nb, x1 - (base * Hkv + kvh * nb)));
+  int piece_ids;
+  {
+    const int us = base * Hkv + kvh * (nb + uc) + uc;
+    piece_ids = load_block_id(p, b, max(x0 - us, 0) + lane, min(nb, x1 - us));
+  }
   while (x < x1) {
     const int ctx = clamp_ctx(p, b);
-    const int ustart = base * Hkv + kvh * nb;  // position of the unit's first block
-    const int j0 = x - ustart;
+    const int ustart = base * Hkv + kvh * (nb + uc) + uc;  // position of the unit's first block
+    const int j0 = max(x - ustart, 0);
     const int j1 = min(nb, x1 - ustart);
     const int h0 = kvh * G;
     const int npairs = (j1 - j0 + 1) / 2;
 
-    // The next piece (it starts at its unit's first block): the next kv head
-    // of b, else the next sequence with blocks.
-    const int xn = ustart + j1;
+    // The next unit (its range starts where this piece ends when the piece
+    // reaches the unit's last block): the next kv head of b, else the next
+    // sequence with blocks. A range that ends inside this unit, or inside its
+    // leading charge (j1 <= 0), ends the loop.
+    const int xn = ustart + max(j1, 0);
     int bn = b, kvhn = kvh + 1, basen = base, nbn = nb;
     if (kvhn == Hkv) {
       kvhn = 0;
-      basen = base + nb;
+      basen = base + nb + uc;
       do {
         ++bn;
       } while (xn < x1 && bn < p.B && nblk_of(clamp_ctx(p, bn)) == 0);
       nbn = (xn < x1) ? nblk_of(clamp_ctx(p, bn)) : 0;
     }
-    const int next_piece_ids = (xn < x1) ? load_block_id(p, bn, lane, min(nbn, x1 - xn)) : -1;
+    const int next_piece_ids = (xn < x1) ? load_block_id(p, bn, lane, min(nbn, x1 - xn - uc)) : -1;
+    if (j1 <= j0) break;  // the range ends inside the unit's leading charge
 
     // q as the B operand of the QK product: column g = r, k = d in [c*32 + qg*8, +8).
     bf16x8 qf[NC];
@@ -438,8 +464,10 @@ static int resident_wgs() {
   return v;
 }
 
+static int unit_cost(const aflex_attn_args& a) { return a.split_tokens > 0 ? 0 : kUnitCost; }
+
 static long long work_bound(const aflex_attn_args& a) {
-  return (long long)a.B * a.Hkv * ((a.max_context_len + 15) / 16);
+  return (long long)a.B * a.Hkv * ((a.max_context_len + 15) / 16 + unit_cost(a));
 }
 
 // Grid size: with a fixed piece size, enough work-groups for the bound on the
@@ -483,6 +511,7 @@ hipError_t launch_attn_decode(const aflex_attn_args& a, void* ws, hipStream_t st
   p.num_blocks = a.num_blocks;
   p.max_ctx = a.max_context_len;
   p.chunk_blocks = a.split_tokens > 0 ? a.split_tokens / 16 : 0;
+  p.unit_cost = unit_cost(a);
   const float scale = a.scale != 0.f ? a.scale : 1.0f / sqrtf((float)a.D);
   p.scale_log2 = scale * kLog2e;
   const int P = attn_grid(a);

@@ -23,7 +23,9 @@
 // Work decomposition: a 1-D grid over (m-tile, n-tile, k-split). Work-groups
 // are dispatched round-robin over the 8 XCDs; the logical tile index is
 // remapped so that consecutive tiles (which share an A tile, or for dense
-// GEMMs a weight tile across m-tiles) land on the same XCD and its L2.
+// GEMMs a weight tile across m-tiles) land on the same XCD and its L2. With a
+// device-side tile map the remap can run over the real tile count instead of
+// the grid (mt_major = 2), so the tiles spread evenly over the XCDs.
 // m-tiles come either from a dense row count or from a device-side tile map
 // of (expert, first row, end row) triples written by the MoE routing kernel;
 // work-groups beyond the map's device-side count exit at once, so the grid is
@@ -51,7 +53,8 @@ struct GemmParams {
   const int32_t* num_mtiles;  // device count of valid tile_map entries
   int max_mtiles;
   int n_ntiles;
-  int mt_major;               // 1: m-tile is the slow index of the tile order
+  int mt_major;               // 1: m-tile is the slow index of the tile order; 2: the same over
+                              // the device-side row-tile count (tile_map only), spread over the XCDs
   uint16_t* C;                // bf16 output [rows, ldc]
   int ldc;
   const uint16_t* R;          // optional bf16 residual [rows, ldc] added before rounding (plain bf16 output only)
@@ -135,7 +138,17 @@ __global__ __launch_bounds__(64 * WM * WN, LDS_BYTES > 81920 ? 1 : 2) void gemm_
   // on distinct bank groups.
   __shared__ __attribute__((aligned(16))) uint16_t sm[STAGES][ROWS * BK];
 
-  const int t = xcd_remap(blockIdx.x, gridDim.x);
+  int t;
+  if (p.mt_major == 2) {
+    // Row tiles from the device-side count, expert-major: the real tiles
+    // spread evenly over the XCDs, each XCD taking consecutive n-tiles of one
+    // or two experts (whose token rows then stay in its L2).
+    const int nreal = *p.num_mtiles * p.n_ntiles * p.splits;
+    if ((int)blockIdx.x >= nreal) return;
+    t = xcd_remap(blockIdx.x, nreal);
+  } else {
+    t = xcd_remap(blockIdx.x, gridDim.x);
+  }
   const int split = t % p.splits;
   const int rest = t / p.splits;
   int mt, nt;

@@ -41,6 +41,24 @@ def test_full_1024_token_splits(gpu_lib, split):
     check_rows(out, _oracle(a), what=f"1024-token splits (split={split})")
 
 
+@pytest.mark.parametrize("seed", [0, 1])
+def test_many_short_units_partition(gpu_lib, seed):
+    """Hundreds of short (sequence, kv head) units between empty sequences and a
+    few long ones: the even split charges every unit a fixed cost besides its
+    blocks, so work-group ranges start and end inside units, inside a unit's
+    charge (no block of it) and across runs of empty sequences."""
+    rng = np.random.default_rng(900 + seed)
+    ctx = rng.integers(1, 49, 300)
+    ctx[rng.random(300) < 0.2] = 0
+    ctx[rng.choice(300, 4, replace=False)] = rng.integers(2000, 6000, 4)
+    a = synth.custom_attention(40 + seed, len(ctx), 32, 8, 128, ctx, ctx_hi=6000)
+    out = aflex.attn_decode(a.to(DEV)).cpu()
+    ref = _oracle(a)
+    nz = torch.from_numpy(ctx > 0)
+    check_rows(out[nz], ref[nz], what=f"many short units (seed {seed})")
+    assert torch.count_nonzero(out[~nz]) == 0
+
+
 def test_qwen3_shape_all_rows(gpu_lib):
     """The Qwen3-32B workload at full size (B = 64, 64/8 heads, lognormal
     contexts): every sequence and head against the oracle."""
