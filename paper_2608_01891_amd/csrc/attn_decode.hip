@@ -422,18 +422,23 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnParams p) {
   for (int it = threadIdx.x; it < G * D4; it += 256) {
     const int g = it / D4;
     const int d4 = it - g * D4;
-    float M = kNegInf;
-#pragma unroll 4
-    for (int w = wf; w <= wl; ++w) M = fmaxf(M, p.part_ml[(((size_t)unit + w) * G + g) * 2]);
-    const float Mu = (M == kNegInf) ? 0.f : M;
-    float L = 0.f;
+    // One pass over the pieces with a running maximum: every piece's loads are
+    // independent of the running state, so they go out together.
+    float M = kNegInf, L = 0.f;
     f32x4 O = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll 4
     for (int w = wf; w <= wl; ++w) {
       const size_t s = (size_t)unit + w;
-      const float wt = fast_exp2(p.part_ml[(s * G + g) * 2] - Mu);
-      L += wt * p.part_ml[(s * G + g) * 2 + 1];
-      O += wt * *reinterpret_cast<const f32x4*>(&p.part_o[(s * G + g) * D + d4 * 4]);
+      const float m = p.part_ml[(s * G + g) * 2];
+      const float l = p.part_ml[(s * G + g) * 2 + 1];
+      const f32x4 o = *reinterpret_cast<const f32x4*>(&p.part_o[(s * G + g) * D + d4 * 4]);
+      const float Mn = fmaxf(M, m);
+      const float Mu = (Mn == kNegInf) ? 0.f : Mn;
+      const float wa = fast_exp2(M - Mu);  // weight of the pieces so far
+      const float wb = fast_exp2(m - Mu);  // weight of piece w
+      L = L * wa + l * wb;
+      O = O * wa + o * wb;
+      M = Mn;
     }
     const float inv = L > 0.f ? 1.f / L : 0.f;
     ushort4 v;

@@ -48,6 +48,8 @@ struct GemmParams {
   long long b_expert_stride;  // elements between experts' weight matrices
   int N, K;
   int k_per_split, splits;
+  int split_slots;            // > 0 (tile map only): the split count is chosen on the device from the
+                              // row-tile count (at most splits) to fill rounds of split_slots work-groups
   int M;                      // dense row count (tile_map == nullptr)
   const int32_t* tile_map;    // [max_mtiles][3] = (expert, row_begin, row_end)
   const int32_t* num_mtiles;  // device count of valid tile_map entries
@@ -106,6 +108,32 @@ __device__ __forceinline__ int xcd_remap(int w, int nwg) {
   return (x < rem ? x * (q + 1) : rem * (q + 1) + (x - rem) * q) + j;
 }
 
+// Split-K count for `tiles` output tiles over K = 64 * ksteps: the smallest
+// count up to smax whose work-groups fill the rounds of `slots` concurrent
+// work-groups they need to at least 90%, else the best-filled one; *kps is the
+// k elements per split (a multiple of 64). The device-side twin of the host
+// planner, used where the row-tile count is known on the device only.
+__device__ __forceinline__ void split_plan_slots(int tiles, int ksteps, int smax, int slots, int* splits, int* kps) {
+  int s = 1;
+  long long bn = 0, bd = 1;  // best fill so far, bn / bd
+  for (int c = 1; c <= smax; ++c) {
+    const long long wgs = (long long)tiles * c;
+    const long long cap = ((wgs + slots - 1) / slots) * slots;
+    if (10 * wgs >= 9 * cap) {
+      s = c;
+      break;
+    }
+    if (wgs * bd > bn * cap) {
+      bn = wgs;
+      bd = cap;
+      s = c;
+    }
+  }
+  const int steps = (ksteps + s - 1) / s;
+  *splits = (ksteps + steps - 1) / steps;
+  *kps = steps * 64;
+}
+
 // BM x BN output tile, WM x WN waves (each a (BM/WM) x (BN/WN) sub-tile of
 // MS x MS MFMA tiles: v_mfma_f32_16x16x32_bf16 or v_mfma_f32_32x32x16_bf16),
 // BK-wide k-steps, LDS_BYTES of LDS per work-group (the ring has as many
@@ -138,19 +166,23 @@ __global__ __launch_bounds__(64 * WM * WN, LDS_BYTES > 81920 ? 1 : 2) void gemm_
   // on distinct bank groups.
   __shared__ __attribute__((aligned(16))) uint16_t sm[STAGES][ROWS * BK];
 
-  int t;
-  if (p.mt_major == 2) {
-    // Row tiles from the device-side count, expert-major: the real tiles
-    // spread evenly over the XCDs, each XCD taking consecutive n-tiles of one
-    // or two experts (whose token rows then stay in its L2).
-    const int nreal = *p.num_mtiles * p.n_ntiles * p.splits;
+  int t, splits = p.splits, kps = p.k_per_split, mrange = p.max_mtiles;
+  if (p.mt_major == 2 || p.split_slots > 0) {
+    // Row tiles from the device-side count (and the split count planned from
+    // it): the real tiles spread evenly over the XCDs. Expert-major
+    // (mt_major = 2), each XCD takes consecutive n-tiles of one or two experts,
+    // whose token rows then stay in its L2.
+    const int mtiles = *p.num_mtiles;
+    if (p.split_slots > 0) split_plan_slots(mtiles * p.n_ntiles, p.K / 64, p.splits, p.split_slots, &splits, &kps);
+    const int nreal = mtiles * p.n_ntiles * splits;
     if ((int)blockIdx.x >= nreal) return;
     t = xcd_remap(blockIdx.x, nreal);
+    mrange = mtiles;
   } else {
     t = xcd_remap(blockIdx.x, gridDim.x);
   }
-  const int split = t % p.splits;
-  const int rest = t / p.splits;
+  const int split = t % splits;
+  const int rest = t / splits;
   int mt, nt;
   if (p.mt_major) {
     nt = rest % p.n_ntiles;
@@ -164,8 +196,8 @@ __global__ __launch_bounds__(64 * WM * WN, LDS_BYTES > 81920 ? 1 : 2) void gemm_
     mt = grp * 8 + in % gm;
     nt = in / gm;
   } else {
-    mt = rest % p.max_mtiles;
-    nt = rest / p.max_mtiles;
+    mt = rest % mrange;
+    nt = rest / mrange;
   }
   int expert = 0, row0, row1;
   if (p.tile_map) {
@@ -178,8 +210,8 @@ __global__ __launch_bounds__(64 * WM * WN, LDS_BYTES > 81920 ? 1 : 2) void gemm_
     row1 = min(row0 + BM, p.M);
   }
   const int n0 = nt * BN;
-  const int kb = split * p.k_per_split;
-  const int ke = min(p.K, kb + p.k_per_split);
+  const int kb = split * kps;
+  const int ke = min(p.K, kb + kps);
   const int nk = (ke - kb) / BK;
 
   const int tid = threadIdx.x;

@@ -302,13 +302,19 @@ __global__ __launch_bounds__(256) void moe_rank_kernel(const int32_t* __restrict
 }
 
 __global__ __launch_bounds__(256) void moe_combine_kernel(const float* __restrict__ P, long long split_stride,
-                                                          int splits, const int32_t* __restrict__ pos,
+                                                          int splits, int split_slots,
+                                                          const int32_t* __restrict__ num_tiles, int n_ntiles,
+                                                          int ksteps, const int32_t* __restrict__ pos,
                                                           const float* __restrict__ w, int k, int H,
                                                           const uint16_t* __restrict__ residual,
                                                           uint16_t* __restrict__ y) {
   const int t = blockIdx.x;
   const int c = (blockIdx.y * 256 + threadIdx.x) * 4;
   if (c >= H) return;
+  if (split_slots > 0) {  // the down GEMM planned its split count on the device
+    int kps;
+    split_plan_slots(*num_tiles * n_ntiles, ksteps, splits, split_slots, &splits, &kps);
+  }
   f32x4 acc = {0.f, 0.f, 0.f, 0.f};
   for (int j = 0; j < k; ++j) {
     const long long row = pos[t * k + j];
@@ -424,6 +430,11 @@ hipError_t launch_moe_experts(const aflex_ffn_args& f, void* route_ws, void* exp
   d.K = f.I;
   d.k_per_split = L.down_kps;
   d.splits = L.down_splits;
+  // One-work-group-per-CU tiles: the split count follows the routed tile
+  // count (at most the worst-case plan's), so whole rounds stay filled
+  // without fp32 partials the tile count does not need (2048 tokens: one
+  // split instead of three).
+  d.split_slots = L.bm >= 128 ? concurrent_wgs(L.bm) : 0;
   d.tile_map = tile_map;
   d.num_mtiles = num_tiles;
   d.max_mtiles = L.max_tiles;
@@ -437,8 +448,8 @@ hipError_t launch_moe_experts(const aflex_ffn_args& f, void* route_ws, void* exp
 
   dim3 grid(f.T, (f.H / 4 + 255) / 256);
   ProfScope ps("moe_combine", stream);
-  moe_combine_kernel<<<grid, 256, 0, stream>>>(P, d.p_split_stride, L.down_splits, pos, wts, f.k, f.H, residual,
-                                               f.y);
+  moe_combine_kernel<<<grid, 256, 0, stream>>>(P, d.p_split_stride, L.down_splits, d.split_slots, num_tiles,
+                                               d.n_ntiles, f.I / 64, pos, wts, f.k, f.H, residual, f.y);
   return hipGetLastError();
 }
 
