@@ -142,7 +142,9 @@ __device__ __forceinline__ int chunk_of(const AttnParams& p, int P, int lane, in
   return p.chunk_blocks ? p.chunk_blocks : max((W + P - 1) / P, kMinChunkBlocks);
 }
 
-template <int D, bool NT>
+// UNIT: one work-group per (sequence, kv head) unit, written whole (no
+// partials); otherwise the even split of the flattened range.
+template <int D, bool NT, bool UNIT>
 __global__ __launch_bounds__(256, 3) void attn_decode_kernel(AttnParams p) {
   constexpr int NC = D / 32;   // k-chunks of the QK product
   constexpr int NMT = D / 16;  // d-tiles of the PV product
@@ -171,35 +173,41 @@ __global__ __launch_bounds__(256, 3) void attn_decode_kernel(AttnParams p) {
   }
 
   // ---- partition: this work-group's range of the flattened blocks ----
-  int W;
-  const int C = chunk_of(p, P, lane, &W);
-  const int x0 = wg * C;
-  if (x0 >= W) return;
-  const int x1 = min(x0 + C, W);
+  // (UNIT: work-group wg takes unit wg = (sequence ub, kv head wg % Hkv), all
+  // of its blocks as one piece, with a chunk no range can span twice.)
+  int W = 0;
+  const int C = UNIT ? (1 << 30) : chunk_of(p, P, lane, &W);
+  const int ub = UNIT ? wg / Hkv : 0;
+  const int unb = UNIT ? (ub < p.B ? nblk_of(clamp_ctx(p, ub)) : 0) : 0;
+  const int x0 = UNIT ? (wg - ub * Hkv) * unb : wg * C;
+  if (UNIT ? unb == 0 : x0 >= W) return;
+  const int x1 = UNIT ? x0 + unb : min(x0 + C, W);
 
   // First sequence whose units reach past x0: base = its first position per
   // kv head. Unit (b, kvh) spans positions [S, S + len) with
   // S = base * Hkv + kvh * len and len = nblk + unit_cost; its block j sits at
   // S + unit_cost + j, so a work-group whose range lies in a unit's leading
   // charge holds no piece of it.
-  int b = 0, base = 0;
-  for (int c = 0; c < p.B; c += 64) {
-    const int bb = c + lane;
-    const int n = bb < p.B ? unit_len(p, bb) : 0;
-    const int incl = wave_incl_scan(n, lane);
-    const unsigned long long past = __ballot((base + incl) * Hkv > x0);
-    if (past) {
-      const int l = __builtin_ctzll(past);
-      b = c + l;
-      base += __builtin_amdgcn_readlane(incl - n, l);
-      break;
+  int b = ub, base = 0;
+  if constexpr (!UNIT) {
+    for (int c = 0; c < p.B; c += 64) {
+      const int bb = c + lane;
+      const int n = bb < p.B ? unit_len(p, bb) : 0;
+      const int incl = wave_incl_scan(n, lane);
+      const unsigned long long past = __ballot((base + incl) * Hkv > x0);
+      if (past) {
+        const int l = __builtin_ctzll(past);
+        b = c + l;
+        base += __builtin_amdgcn_readlane(incl - n, l);
+        break;
+      }
+      base += __builtin_amdgcn_readlane(incl, 63);
     }
-    base += __builtin_amdgcn_readlane(incl, 63);
   }
   // (every value that steers the piece loop is wave-uniform: scalar registers)
   b = __builtin_amdgcn_readfirstlane(b);
   base = __builtin_amdgcn_readfirstlane(base);
-  const int uc = p.unit_cost;
+  const int uc = UNIT ? 0 : p.unit_cost;
   int nb = nblk_of(clamp_ctx(p, b));
   int kvh = (x0 - base * Hkv) / (nb + uc);
 
@@ -475,10 +483,22 @@ static long long work_bound(const aflex_attn_args& a) {
   return (long long)a.B * a.Hkv * ((a.max_context_len + 15) / 16 + unit_cost(a));
 }
 
-// Grid size: with a fixed piece size, enough work-groups for the bound on the
-// blocks; otherwise the resident work-groups, fewer when the bound cannot give
-// each of them a pair per wave.
+// Contexts of at most this many tokens take one work-group per (sequence, kv
+// head) unit when the units fit in one round of resident work-groups: each
+// unit is written directly (no partials) and the merge launch, which at these
+// sizes costs more than the imbalance between units, is skipped.
+constexpr int kUnitPerWgMaxCtx = 512;
+
+static bool unit_per_wg(const aflex_attn_args& a) {
+  return a.split_tokens == 0 && a.max_context_len <= kUnitPerWgMaxCtx && (long long)a.B * a.Hkv <= resident_wgs();
+}
+
+// Grid size: one work-group per unit for short contexts (above); with a fixed
+// piece size, enough work-groups for the bound on the blocks; otherwise the
+// resident work-groups, fewer when the bound cannot give each of them a pair
+// per wave.
 static int attn_grid(const aflex_attn_args& a) {
+  if (unit_per_wg(a)) return a.B * a.Hkv > 0 ? a.B * a.Hkv : 1;
   const long long wb = work_bound(a);
   long long P;
   if (a.split_tokens > 0) {
@@ -517,6 +537,7 @@ hipError_t launch_attn_decode(const aflex_attn_args& a, void* ws, hipStream_t st
   p.max_ctx = a.max_context_len;
   p.chunk_blocks = a.split_tokens > 0 ? a.split_tokens / 16 : 0;
   p.unit_cost = unit_cost(a);
+  const bool unit = unit_per_wg(a);
   const float scale = a.scale != 0.f ? a.scale : 1.0f / sqrtf((float)a.D);
   p.scale_log2 = scale * kLog2e;
   const int P = attn_grid(a);
@@ -531,12 +552,19 @@ hipError_t launch_attn_decode(const aflex_attn_args& a, void* ws, hipStream_t st
   p.span = reinterpret_cast<int2*>(w);
   {
     ProfScope ps("attn_decode", stream);
-    if (a.D == 128)
-      attn_decode_kernel<128, true><<<P, 256, 0, stream>>>(p);
-    else
-      attn_decode_kernel<64, true><<<P, 256, 0, stream>>>(p);
+    if (a.D == 128) {
+      if (unit)
+        attn_decode_kernel<128, true, true><<<P, 256, 0, stream>>>(p);
+      else
+        attn_decode_kernel<128, true, false><<<P, 256, 0, stream>>>(p);
+    } else {
+      if (unit)
+        attn_decode_kernel<64, true, true><<<P, 256, 0, stream>>>(p);
+      else
+        attn_decode_kernel<64, true, false><<<P, 256, 0, stream>>>(p);
+    }
   }
-  if (P > 1) {  // with one work-group no unit is split
+  if (P > 1 && !unit) {  // with one work-group, or one per unit, no unit is split
     ProfScope ps("attn_merge", stream);
     if (a.D == 128)
       attn_merge_kernel<128><<<a.B * a.Hkv, 256, 0, stream>>>(p);

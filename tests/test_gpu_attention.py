@@ -59,6 +59,22 @@ def test_many_short_units_partition(gpu_lib, seed):
     assert torch.count_nonzero(out[~nz]) == 0
 
 
+@pytest.mark.parametrize("B,Hkv,hi", [(96, 8, 512), (5, 2, 40), (97, 8, 512)])
+def test_short_contexts_one_unit_per_work_group(gpu_lib, B, Hkv, hi):
+    """Contexts up to 512 tokens with every (sequence, kv head) unit in one
+    round of resident work-groups (96 x 8 units on 768) take one work-group per
+    unit and no merge launch; 97 x 8 units fall back to the even split."""
+    rng = np.random.default_rng(950 + B)
+    ctx = rng.integers(1, hi + 1, B)
+    ctx[rng.random(B) < 0.15] = 0
+    ctx[0] = hi
+    a = synth.custom_attention(60 + B, B, 4 * Hkv, Hkv, 128, ctx, ctx_hi=hi)
+    out = aflex.attn_decode(a.to(DEV)).cpu()
+    nz = torch.from_numpy(ctx > 0)
+    check_rows(out[nz], _oracle(a)[nz], what=f"short contexts B={B} Hkv={Hkv}")
+    assert torch.count_nonzero(out[~nz]) == 0
+
+
 def test_qwen3_shape_all_rows(gpu_lib):
     """The Qwen3-32B workload at full size (B = 64, 64/8 heads, lognormal
     contexts): every sequence and head against the oracle."""

@@ -55,6 +55,30 @@ def test_ties_in_logits(gpu_lib):
     assert ids[1].tolist() == [0, 1] and ids[0].tolist() == [3, 0]
 
 
+def test_ties_and_infinities_across_logit_chunks(gpu_lib):
+    """40 experts (the top-k pass reads logits 16 at a time): equal values
+    across chunk boundaries keep the lower ids, -inf logits are taken only
+    after every finite one, in id order."""
+    T, H, I, E, k = 6, 64, 64, 40, 8
+    x, w, _ = synth.custom_ffn(72, T, H, I, E=E)
+    logits = torch.zeros(T, E)
+    logits[0, [33, 17]] = 1.0
+    logits[1, :] = float("-inf")
+    logits[1, 30] = 0.0
+    logits[2, :37] = float("-inf")
+    logits[3, 15:18] = 2.0
+    logits[4, ::5] = -1.0
+    logits[5] = torch.arange(E, dtype=torch.float32).remainder(3)
+    y, r = aflex.moe_ffn(x.to(DEV), w.to(DEV), logits.to(DEV), k, routing=True)
+    ids = _check_routing(r, logits, k, E)
+    assert ids[0].tolist() == [17, 33, 0, 1, 2, 3, 4, 5]
+    assert ids[1].tolist() == [30, 0, 1, 2, 3, 4, 5, 6]
+    assert ids[2].tolist() == [37, 38, 39, 0, 1, 2, 3, 4]
+    assert ids[3].tolist() == [15, 16, 17, 0, 1, 2, 3, 4]
+    assert ids[4].tolist() == [1, 2, 3, 4, 6, 7, 8, 9]
+    assert ids[5].tolist() == [2, 5, 8, 11, 14, 17, 20, 23]
+
+
 @pytest.fixture(scope="module")
 def mixtral():
     wl = synth.mixtral_moe(device=DEV)
