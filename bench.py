@@ -81,9 +81,13 @@ def timed(fn, reps, stream=None):
     return e0.elapsed_time(e1) / reps
 
 
-def timed_kernels(fn, reps, names, aflex):
-    """(ms per call without profiling events, {kernel: avg ms} from a separate profiled pass)."""
-    ms = timed(fn, reps)
+def timed_kernels(fn, reps, names, aflex, warmup=3, windows=3):
+    """(ms per call without profiling events: the median of `windows` windows of
+    `reps` calls after `warmup` untimed calls, {kernel: avg ms} from a separate
+    profiled pass)."""
+    for _ in range(warmup):
+        fn()
+    ms = sorted(timed(fn, reps) for _ in range(windows))[windows // 2]
     aflex.profile_start(names)
     for _ in range(max(3, reps // 3)):
         fn()
