@@ -144,14 +144,15 @@ __device__ __forceinline__ int chunk_of(const AttnParams& p, int P, int lane, in
 
 // UNIT: one work-group per (sequence, kv head) unit, written whole (no
 // partials); otherwise the even split of the flattened range.
-template <int D, bool NT, bool UNIT>
-__global__ __launch_bounds__(256, 3) void attn_decode_kernel(AttnParams p) {
+template <int D, bool NT, bool UNIT, int NW = kWaves>
+__global__ __launch_bounds__(64 * NW, 12 / NW) void attn_decode_kernel(AttnParams p) {
   constexpr int NC = D / 32;   // k-chunks of the QK product
   constexpr int NMT = D / 16;  // d-tiles of the PV product
   constexpr int LDO = D + 4;   // padded row of the LDS merge buffer
 
-  __shared__ float sm_ml[kWaves][2][16];
-  __shared__ __attribute__((aligned(16))) float sm_o[kWaves][16][LDO];
+  constexpr int NT_ = 64 * NW;  // threads
+  __shared__ float sm_ml[NW][2][16];
+  __shared__ __attribute__((aligned(16))) float sm_o[NW][16][LDO];
 
   const int tid = threadIdx.x;
   const int wave = tid >> 6;
@@ -168,7 +169,7 @@ __global__ __launch_bounds__(256, 3) void attn_decode_kernel(AttnParams p) {
   for (int b = wg; b < p.B; b += P) {
     if (clamp_ctx(p, b) == 0) {
       uint4* o = reinterpret_cast<uint4*>(p.out + (size_t)b * p.Hq * D);
-      for (int i = tid; i < p.Hq * D / 8; i += 256) o[i] = make_uint4(0, 0, 0, 0);
+      for (int i = tid; i < p.Hq * D / 8; i += NT_) o[i] = make_uint4(0, 0, 0, 0);
     }
   }
 
@@ -278,7 +279,7 @@ __global__ __launch_bounds__(256, 3) void attn_decode_kernel(AttnParams p) {
 #pragma unroll
     for (int mt = 0; mt < NMT; ++mt) acc[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-    for (int pr = (wave - rot) & (kWaves - 1); pr < npairs; pr += kWaves) {
+    for (int pr = (int)((unsigned)(wave - rot + NW) % NW); pr < npairs; pr += NW) {
       if ((pr >> 5) != cur_chunk) {  // advances by at most one chunk per step
         cur_chunk = pr >> 5;
         my_id = next_id;
@@ -377,16 +378,16 @@ __global__ __launch_bounds__(256, 3) void attn_decode_kernel(AttnParams p) {
     const size_t seg = (size_t)unit + wg;
     if (tid == 0 && wg == wg_first) p.span[unit] = make_int2(wg_first, wg_last);
 
-    for (int it = tid; it < G * D; it += 256) {
+    for (int it = tid; it < G * D; it += NT_) {
       const int g = it / D;
       const int d = it - g * D;
       float M = sm_ml[0][0][g];
 #pragma unroll
-      for (int w = 1; w < kWaves; ++w) M = fmaxf(M, sm_ml[w][0][g]);
+      for (int w = 1; w < NW; ++w) M = fmaxf(M, sm_ml[w][0][g]);
       const float Mu = (M == kNegInf) ? 0.f : M;
       float L = 0.f, O = 0.f;
 #pragma unroll
-      for (int w = 0; w < kWaves; ++w) {
+      for (int w = 0; w < NW; ++w) {
         const float wt = fast_exp2(sm_ml[w][0][g] - Mu);
         L += wt * sm_ml[w][1][g];
         O += wt * sm_o[w][g][d];
@@ -402,7 +403,7 @@ __global__ __launch_bounds__(256, 3) void attn_decode_kernel(AttnParams p) {
       }
     }
 
-    rot = (rot + npairs) & (kWaves - 1);
+    rot = (int)((unsigned)(rot + npairs) % NW);
 
     x = xn;
     b = bn;
@@ -477,6 +478,14 @@ static int resident_wgs() {
   return v;
 }
 
+// Waves of the work-groups of the even split when it runs beside other work
+// on the GPU (the two-stream steps): one 12-wave work-group per CU, its LDS
+// merge buffers (103 KiB) leaving a CU to either attention or FFN work. Alone,
+// three 4-wave work-groups per CU are faster (Qwen3-32B B = 64: 63.2 against
+// 63.9 us); beside the FFN stream the wide form took the pipeline step from
+// 2.71 to 2.67 ms.
+constexpr int kWideWaves = 12;
+
 static int unit_cost(const aflex_attn_args& a) { return a.split_tokens > 0 ? 0 : kUnitCost; }
 
 static long long work_bound(const aflex_attn_args& a) {
@@ -497,12 +506,16 @@ static bool unit_per_wg(const aflex_attn_args& a) {
 // piece size, enough work-groups for the bound on the blocks; otherwise the
 // resident work-groups, fewer when the bound cannot give each of them a pair
 // per wave.
-static int attn_grid(const aflex_attn_args& a) {
+static int attn_grid(const aflex_attn_args& a, bool wide = false) {
   if (unit_per_wg(a)) return a.B * a.Hkv > 0 ? a.B * a.Hkv : 1;
   const long long wb = work_bound(a);
   long long P;
   if (a.split_tokens > 0) {
     P = (wb + a.split_tokens / 16 - 1) / (a.split_tokens / 16);
+  } else if (wide) {  // one wide work-group per CU, a pair per wave at least
+    const int ncu = resident_wgs() / 3;
+    P = (wb + kMinChunkBlocks * 3 - 1) / (kMinChunkBlocks * 3);
+    P = P < ncu ? P : ncu;
   } else {
     P = (wb + kMinChunkBlocks - 1) / kMinChunkBlocks;
     P = P < resident_wgs() ? P : resident_wgs();
@@ -512,6 +525,7 @@ static int attn_grid(const aflex_attn_args& a) {
 
 bool attn_shape_fits(const aflex_attn_args& a) { return work_bound(a) < (1ll << 30); }
 
+// (sized for the narrow grid, which is never smaller than the wide one)
 size_t attn_workspace_bytes(const aflex_attn_args& a) {
   const size_t U = (size_t)a.B * a.Hkv;
   const size_t segs = U + (size_t)attn_grid(a);
@@ -520,7 +534,7 @@ size_t attn_workspace_bytes(const aflex_attn_args& a) {
          align_up(U * sizeof(int2), 256);
 }
 
-hipError_t launch_attn_decode(const aflex_attn_args& a, void* ws, hipStream_t stream) {
+hipError_t launch_attn_decode(const aflex_attn_args& a, void* ws, hipStream_t stream, bool wide) {
   AttnParams p;
   p.q = a.q;
   p.kc = a.k_cache;
@@ -538,9 +552,10 @@ hipError_t launch_attn_decode(const aflex_attn_args& a, void* ws, hipStream_t st
   p.chunk_blocks = a.split_tokens > 0 ? a.split_tokens / 16 : 0;
   p.unit_cost = unit_cost(a);
   const bool unit = unit_per_wg(a);
+  wide = wide && !unit && a.split_tokens == 0;
   const float scale = a.scale != 0.f ? a.scale : 1.0f / sqrtf((float)a.D);
   p.scale_log2 = scale * kLog2e;
-  const int P = attn_grid(a);
+  const int P = attn_grid(a, wide);
   const size_t U = (size_t)a.B * a.Hkv;
   const size_t segs = U + (size_t)P;
   const size_t G = (size_t)p.G;
@@ -555,11 +570,15 @@ hipError_t launch_attn_decode(const aflex_attn_args& a, void* ws, hipStream_t st
     if (a.D == 128) {
       if (unit)
         attn_decode_kernel<128, true, true><<<P, 256, 0, stream>>>(p);
+      else if (wide)
+        attn_decode_kernel<128, true, false, kWideWaves><<<P, 64 * kWideWaves, 0, stream>>>(p);
       else
         attn_decode_kernel<128, true, false><<<P, 256, 0, stream>>>(p);
     } else {
       if (unit)
         attn_decode_kernel<64, true, true><<<P, 256, 0, stream>>>(p);
+      else if (wide)
+        attn_decode_kernel<64, true, false, kWideWaves><<<P, 64 * kWideWaves, 0, stream>>>(p);
       else
         attn_decode_kernel<64, true, false><<<P, 256, 0, stream>>>(p);
     }
