@@ -8,15 +8,18 @@
 // Design (HBM-bound: every cached K/V byte is read exactly once, in one
 // launch):
 //  * Work partition. The (sequence, kv head) units are laid end to end in
-//    (b, kv head) order, each as its ceil(ctx_b / 16) blocks; work-group i of
-//    the grid takes blocks [i C, (i+1) C) of that flattened range, with C the
-//    range divided evenly over the grid (or a fixed size the caller asks
-//    for). Every work-group computes the partition itself from the context
-//    lengths (no host synchronisation, no extra launch), so all of them
-//    stream the same number of bytes and finish together; a work-group's
-//    range is one or more pieces, each the part of one unit that falls into
-//    it.
-//  * Piece kernel body: 4 waves take pairs of 16-token blocks round-robin.
+//    (b, kv head) order, each as its ceil(ctx_b / 16) blocks plus a fixed
+//    charge for the piece it adds; work-group i of the grid takes positions
+//    [i C, (i+1) C) of that flattened range, with C the range divided evenly
+//    over the grid (or a fixed size the caller asks for). Every work-group
+//    computes the partition itself from the context lengths (no host
+//    synchronisation, no extra launch), so all of them stream about the same
+//    number of bytes; a work-group's range is one or more pieces, each the
+//    part of one unit that falls into it. The grid is the resident
+//    work-groups: three 4-wave ones per CU, or one 12-wave one per CU for
+//    calls beside other GPU work. Short contexts take one work-group per
+//    unit instead.
+//  * Piece kernel body: the waves take pairs of 16-token blocks round-robin.
 //    Per pair a wave issues 16 (D=128) 16-byte loads per lane straight into
 //    MFMA operand registers -- no LDS staging is needed because both
 //    contractions see their operand with the contraction index contiguous:
@@ -30,7 +33,7 @@
 //    registers of a lane are exactly the P^T operand registers it needs for
 //    the PV product, and all softmax state of head g lives in the four lanes
 //    with lane % 16 == g: the online softmax needs two cross-lane max steps per
-//    block pair and no LDS round trip. The 4 waves then merge through LDS.
+//    block pair and no LDS round trip. The waves then merge through LDS.
 //  * Merge. A unit held by one piece writes its bf16 output directly. A unit
 //    cut into several pieces (consecutive work-groups; only the first and the
 //    last piece of a work-group's range can be such a piece) has each piece
