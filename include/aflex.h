@@ -98,7 +98,10 @@ typedef struct aflex_attn_args {
  * nothing (their tokens are masked). Two launches on the stream: the split
  * attention, then a merge of the (sequence, kv head) pairs it split between
  * work-groups; the workspace holds their fp32 partials and needs no
- * initialisation. */
+ * initialisation. With split_tokens = 0, max_context_len <= 512 and B * Hkv
+ * at most the resident work-groups, each pair takes one work-group whole and
+ * the merge launch is skipped. The output is the same on every call with the
+ * same inputs (bitwise). */
 aflex_status aflex_attn_decode_workspace(const aflex_attn_args *a, size_t *bytes);
 aflex_status aflex_attn_decode(const aflex_attn_args *a, void *workspace, size_t workspace_bytes,
                                aflex_stream stream);
