@@ -482,11 +482,12 @@ static int resident_wgs() {
 }
 
 // Waves of the work-groups of the even split when it runs beside other work
-// on the GPU (the two-stream steps): one 12-wave work-group per CU, its LDS
+// on the GPU (the pipeline step): one 12-wave work-group per CU, its LDS
 // merge buffers (103 KiB) leaving a CU to either attention or FFN work. Alone,
 // three 4-wave work-groups per CU are faster (Qwen3-32B B = 64: 63.2 against
 // 63.9 us); beside the FFN stream the wide form took the pipeline step from
-// 2.71 to 2.67 ms.
+// 2.71 to 2.67 ms. The layer step, whose attention stream also runs o_proj,
+// is faster with the 4-wave form (2.742 against 2.768 ms).
 constexpr int kWideWaves = 12;
 
 static int unit_cost(const aflex_attn_args& a) { return a.split_tokens > 0 ? 0 : kUnitCost; }

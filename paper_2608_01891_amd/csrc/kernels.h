@@ -23,8 +23,8 @@ size_t attn_workspace_bytes(const aflex_attn_args& a);
 // K/V tiles stream with non-temporal loads: every cached byte is read once,
 // alone and next to the FFN's weight stream in the two-stream step alike
 // (that step: 2.785 -> 2.730 ms against ordinary loads). wide: the even split
-// in one 12-wave work-group per CU, for calls that run beside other GPU work
-// (the two-stream steps); the workspace is the same.
+// in one 12-wave work-group per CU, for calls that run beside the FFN's
+// weight stream (the pipeline step); the workspace is the same.
 hipError_t launch_attn_decode(const aflex_attn_args& a, void* ws, hipStream_t stream, bool wide = false);
 
 // Dense SwiGLU FFN (ffn.hip).
