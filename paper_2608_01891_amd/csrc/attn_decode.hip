@@ -9,16 +9,17 @@
 // launch):
 //  * Work partition. The (sequence, kv head) units are laid end to end in
 //    (b, kv head) order, each as its ceil(ctx_b / 16) blocks plus a fixed
-//    charge for the piece it adds; work-group i of the grid takes positions
-//    [i C, (i+1) C) of that flattened range, with C the range divided evenly
-//    over the grid (or a fixed size the caller asks for). Every work-group
+//    charge for the piece it adds; the work-groups take consecutive ranges of
+//    that flattened range in work-group order: equal ones (or a fixed size
+//    the caller asks for), except that in the grid of three work-groups per
+//    CU the three dispatch rounds take ranges weighted 5:3:1, since the
+//    first work-group dispatched to a CU progresses fastest. Every work-group
 //    computes the partition itself from the context lengths (no host
-//    synchronisation, no extra launch), so all of them stream about the same
-//    number of bytes; a work-group's range is one or more pieces, each the
-//    part of one unit that falls into it. The grid is the resident
-//    work-groups: three 4-wave ones per CU, or one 12-wave one per CU for
-//    calls beside other GPU work. Short contexts take one work-group per
-//    unit instead.
+//    synchronisation, no extra launch); a work-group's range is one or more
+//    pieces, each the part of one unit that falls into it. The grid is the
+//    resident work-groups: three 4-wave ones per CU, or one 12-wave one per
+//    CU for calls beside other GPU work. Short contexts take one work-group
+//    per unit instead.
 //  * Piece kernel body: the waves take pairs of 16-token blocks round-robin.
 //    Per pair a wave issues 16 (D=128) 16-byte loads per lane straight into
 //    MFMA operand registers -- no LDS staging is needed because both
@@ -33,7 +34,11 @@
 //    registers of a lane are exactly the P^T operand registers it needs for
 //    the PV product, and all softmax state of head g lives in the four lanes
 //    with lane % 16 == g: the online softmax needs two cross-lane max steps per
-//    block pair and no LDS round trip. The waves then merge through LDS.
+//    block pair and no LDS round trip. At a piece's end each wave deposits
+//    its partial in an LDS slot (a ring of two for G <= 8) and goes on to the
+//    next piece; the wave that deposits last merges the piece's partials in
+//    wave order, so no wave waits at a barrier for the one with an extra pair
+//    and the result does not depend on which wave merges.
 //  * Merge. A unit held by one piece writes its bf16 output directly. A unit
 //    cut into several pieces (consecutive work-groups; only the first and the
 //    last piece of a work-group's range can be such a piece) has each piece
@@ -67,6 +72,7 @@ struct AttnParams {
   int max_blocks, num_blocks, max_ctx;
   int chunk_blocks;              // > 0: fixed blocks per work-group; 0: even split over the grid
   int unit_cost;                 // extra cost of a unit in block positions (0 with fixed pieces)
+  int rounds;                    // 3: range sizes weighted by dispatch round (see split_of); else 1
   float scale_log2;              // softmax scale * log2(e)
 };
 
@@ -145,6 +151,60 @@ __device__ __forceinline__ int chunk_of(const AttnParams& p, int P, int lane, in
   return p.chunk_blocks ? p.chunk_blocks : max((W + P - 1) / P, kMinChunkBlocks);
 }
 
+// Relative range sizes of the three work-groups that share a CU in the
+// resident grid, by dispatch round (work-groups [0, P/3) are dispatched
+// first, one per CU, then the next P/3). With equal ranges the first
+// work-group on a CU ends first and the third last (Qwen3-32B B = 64: 35.7,
+// 44.2 and 52.0 us on average, the same placement and order in every run):
+// the older waves win the CU's arbitration. Weighting the ranges by round
+// shortens the launch (Qwen3-32B B = 64, uniform / 6:5:4 / 4:3:2 / 5:3:1 /
+// 6:3:1 / 3:2:0: 63.3 / 63.1 / 62.4 / 61.8 / 61.8 / 63.1 us; long-context
+// B = 256: 871 -> 868 us with 5:3:1).
+constexpr int kRoundWeight[3] = {5, 3, 1};
+
+// Ranges of the work-groups: wg = k R + i (round k < rounds, 0 <= i < R) takes
+// c_k positions, the ranges laid end to end in work-group order. (Plain
+// scalars, not a struct: a struct here was kept in per-thread LDS copies.)
+__device__ __forceinline__ void split_of(const AttnParams& p, int P, int W, int C, int& R, int& c0, int& c1,
+                                         int& c2) {
+  if (p.rounds == 3 && p.chunk_blocks == 0) {
+    // rounds 0 and 1 from the weights, round 2 the rest (so the ranges cover W)
+    R = P / 3;
+    const float per = (float)W / (float)(R * (kRoundWeight[0] + kRoundWeight[1] + kRoundWeight[2]));
+    c0 = max((int)(per * kRoundWeight[0]), kMinChunkBlocks);
+    c1 = max((int)(per * kRoundWeight[1]), kMinChunkBlocks);
+    const int rest = W - R * (c0 + c1);
+    c2 = max((rest + R - 1) / R, kMinChunkBlocks);
+  } else {
+    R = P;
+    c0 = c1 = c2 = C;
+  }
+  R = __builtin_amdgcn_readfirstlane(R);
+  c0 = __builtin_amdgcn_readfirstlane(c0);
+  c1 = __builtin_amdgcn_readfirstlane(c1);
+  c2 = __builtin_amdgcn_readfirstlane(c2);
+}
+
+__device__ __forceinline__ int split_start(int R, int c0, int c1, int c2, int wg) {
+  const int k = wg / R;
+  const int i = wg - k * R;
+  return (k > 0 ? R * c0 : 0) + (k > 1 ? R * c1 : 0) + i * (k == 0 ? c0 : k == 1 ? c1 : c2);
+}
+
+__device__ __forceinline__ int split_size(int R, int c0, int c1, int c2, int wg) {
+  const int k = wg / R;
+  return k == 0 ? c0 : k == 1 ? c1 : c2;
+}
+
+// Work-group whose range holds position x (x below the total).
+__device__ __forceinline__ int split_owner(int R, int c0, int c1, int c2, int x) {
+  const int e0 = R * c0;
+  if (x < e0) return x / c0;
+  const int e1 = e0 + R * c1;
+  if (x < e1) return R + (x - e0) / c1;
+  return 2 * R + (x - e1) / c2;
+}
+
 // UNIT: one work-group per (sequence, kv head) unit, written whole (no
 // partials); otherwise the even split of the flattened range.
 template <int D, bool NT, bool UNIT, int NW = kWaves>
@@ -154,8 +214,14 @@ __global__ __launch_bounds__(64 * NW, 12 / NW) void attn_decode_kernel(AttnParam
   constexpr int LDO = D + 4;   // padded row of the LDS merge buffer
 
   constexpr int NT_ = 64 * NW;  // threads
-  __shared__ float sm_ml[NW][2][16];
-  __shared__ __attribute__((aligned(16))) float sm_o[NW][16][LDO];
+  // Piece partials of the waves, in a ring of LDS slots: two slots of 8 head
+  // rows per wave when G <= 8, else one slot of 16 rows (the same bytes).
+  // Per slot, arrive counts the waves that deposited the current piece and
+  // gen counts the pieces merged out of it.
+  __shared__ float sm_ml[NW * 16 * 2];
+  __shared__ __attribute__((aligned(16))) float sm_o[NW * 16 * LDO];
+  __shared__ int sm_arrive[2];
+  __shared__ int sm_gen[2];
 
   const int tid = threadIdx.x;
   const int wave = tid >> 6;
@@ -166,6 +232,14 @@ __global__ __launch_bounds__(64 * NW, 12 / NW) void attn_decode_kernel(AttnParam
   const int Hkv = p.Hkv;
   const int wg = blockIdx.x;
   const int P = gridDim.x;
+  const int GR = G <= 8 ? 8 : 16;     // head rows of a slot
+  const int nslot = G <= 8 ? 2 : 1;
+
+  if (tid < 2) {
+    sm_arrive[tid] = 0;
+    sm_gen[tid] = 0;
+  }
+  __syncthreads();
 
   // Sequences with no cached token produce zeros; work-group wg clears those
   // with b = wg (mod P).
@@ -180,12 +254,20 @@ __global__ __launch_bounds__(64 * NW, 12 / NW) void attn_decode_kernel(AttnParam
   // (UNIT: work-group wg takes unit wg = (sequence ub, kv head wg % Hkv), all
   // of its blocks as one piece, with a chunk no range can span twice.)
   int W = 0;
-  const int C = UNIT ? (1 << 30) : chunk_of(p, P, lane, &W);
+  int sR = P, sc0 = 1 << 30, sc1 = 1 << 30, sc2 = 1 << 30;
+  if constexpr (!UNIT) {
+    const int C = chunk_of(p, P, lane, &W);
+    if constexpr (NW == kWaves) {  // the grid of three work-groups per CU
+      split_of(p, P, W, C, sR, sc0, sc1, sc2);
+    } else {
+      sc0 = sc1 = sc2 = C;
+    }
+  }
   const int ub = UNIT ? wg / Hkv : 0;
   const int unb = UNIT ? (ub < p.B ? nblk_of(clamp_ctx(p, ub)) : 0) : 0;
-  const int x0 = UNIT ? (wg - ub * Hkv) * unb : wg * C;
+  const int x0 = __builtin_amdgcn_readfirstlane(UNIT ? (wg - ub * Hkv) * unb : split_start(sR, sc0, sc1, sc2, wg));
   if (UNIT ? unb == 0 : x0 >= W) return;
-  const int x1 = UNIT ? x0 + unb : min(x0 + C, W);
+  const int x1 = __builtin_amdgcn_readfirstlane(UNIT ? x0 + unb : min(x0 + split_size(sR, sc0, sc1, sc2, wg), W));
 
   // First sequence whose units reach past x0: base = its first position per
   // kv head. Unit (b, kvh) spans positions [S, S + len) with
@@ -229,6 +311,7 @@ __global__ __launch_bounds__(64 * NW, 12 / NW) void attn_decode_kernel(AttnParam
   int rot = 0;  // wave that takes the piece's first pair: spreads the odd pairs over the waves
 
   int x = x0;
+  int piece = 0;  // pieces this work-group has finished
   // First block-id chunk of the current piece; each piece loads the next
   // piece's first chunk while it streams, so a new piece starts with its K/V
   // loads instead of a round trip for its block ids.
@@ -363,48 +446,77 @@ __global__ __launch_bounds__(64 * NW, 12 / NW) void attn_decode_kernel(AttnParam
     l_run += __shfl_xor(l_run, 16);
     l_run += __shfl_xor(l_run, 32);
 
-    __syncthreads();  // the previous piece's readers of the LDS buffers are done
-    if (qg == 0) {
-      sm_ml[wave][0][r] = m_run;
-      sm_ml[wave][1][r] = l_run;
-    }
-#pragma unroll
-    for (int mt = 0; mt < NMT; ++mt)
-      *reinterpret_cast<f32x4*>(&sm_o[wave][r][mt * 16 + 4 * qg]) = acc[mt];
-    __syncthreads();
-
-    // Work-groups holding pieces of this unit; the one with its first piece
-    // records the span for the merge launch.
-    const int wg_first = ustart / C;
-    const int wg_last = (ustart + nb - 1) / C;
-    const int unit = b * Hkv + kvh;
-    const size_t seg = (size_t)unit + wg;
-    if (tid == 0 && wg == wg_first) p.span[unit] = make_int2(wg_first, wg_last);
-
-    for (int it = tid; it < G * D; it += NT_) {
-      const int g = it / D;
-      const int d = it - g * D;
-      float M = sm_ml[0][0][g];
-#pragma unroll
-      for (int w = 1; w < NW; ++w) M = fmaxf(M, sm_ml[w][0][g]);
-      const float Mu = (M == kNegInf) ? 0.f : M;
-      float L = 0.f, O = 0.f;
-#pragma unroll
-      for (int w = 0; w < NW; ++w) {
-        const float wt = fast_exp2(sm_ml[w][0][g] - Mu);
-        L += wt * sm_ml[w][1][g];
-        O += wt * sm_o[w][g][d];
+    // Deposit this wave's partial in the piece's slot once the slot's previous
+    // piece has been merged out of it; the wave that deposits last merges the
+    // piece. No wave waits for the others at a piece boundary: the ones done
+    // with their pairs go on to the next piece's loads.
+    const int slot = piece & (nslot - 1);
+    const int use = piece / nslot;
+    while (__hip_atomic_load(&sm_gen[slot], __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP) != use)
+      __builtin_amdgcn_s_sleep(1);
+    float* so = sm_o + (slot * NW * GR) * LDO;
+    float* sml = sm_ml + slot * NW * GR * 2;
+    if (r < G) {
+      if (qg == 0) {
+        sml[(wave * GR + r) * 2 + 0] = m_run;
+        sml[(wave * GR + r) * 2 + 1] = l_run;
       }
-      if (wg_first == wg_last) {
-        p.out[((size_t)b * p.Hq + h0 + g) * D + d] = f2bf(L > 0.f ? O / L : 0.f);
-      } else {
-        p.part_o[(seg * G + g) * D + d] = O;
-        if (d == 0) {
-          p.part_ml[(seg * G + g) * 2 + 0] = M;
-          p.part_ml[(seg * G + g) * 2 + 1] = L;
+#pragma unroll
+      for (int mt = 0; mt < NMT; ++mt)
+        *reinterpret_cast<f32x4*>(&so[(wave * GR + r) * LDO + mt * 16 + 4 * qg]) = acc[mt];
+    }
+    int arrived = 0;
+    if (lane == 0)
+      arrived = __hip_atomic_fetch_add(&sm_arrive[slot], 1, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_WORKGROUP);
+    arrived = __builtin_amdgcn_readfirstlane(arrived);
+
+    if (arrived == NW - 1) {
+      // Work-groups holding pieces of this unit; the one with its first piece
+      // records the span for the merge launch.
+      const int wg_first = UNIT ? 0 : split_owner(sR, sc0, sc1, sc2, ustart);
+      const int wg_last = UNIT ? 0 : split_owner(sR, sc0, sc1, sc2, ustart + nb - 1);
+      const int unit = b * Hkv + kvh;
+      const size_t seg = (size_t)unit + wg;
+      if (lane == 0 && wg == wg_first) p.span[unit] = make_int2(wg_first, wg_last);
+
+      constexpr int D4 = D / 4;
+      for (int it = lane; it < G * D4; it += 64) {
+        const int g = it / D4;
+        const int d4 = it - g * D4;
+        float M = sml[g * 2];
+#pragma unroll
+        for (int w = 1; w < NW; ++w) M = fmaxf(M, sml[(w * GR + g) * 2]);
+        const float Mu = (M == kNegInf) ? 0.f : M;
+        float L = 0.f;
+        f32x4 O = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll 2
+        for (int w = 0; w < NW; ++w) {
+          const float wt = fast_exp2(sml[(w * GR + g) * 2] - Mu);
+          L += wt * sml[(w * GR + g) * 2 + 1];
+          O += wt * *reinterpret_cast<const f32x4*>(&so[(w * GR + g) * LDO + d4 * 4]);
+        }
+        if (wg_first == wg_last) {
+          ushort4 v;
+          v.x = f2bf(L > 0.f ? O[0] / L : 0.f);
+          v.y = f2bf(L > 0.f ? O[1] / L : 0.f);
+          v.z = f2bf(L > 0.f ? O[2] / L : 0.f);
+          v.w = f2bf(L > 0.f ? O[3] / L : 0.f);
+          *reinterpret_cast<ushort4*>(p.out + ((size_t)b * p.Hq + h0 + g) * D + d4 * 4) = v;
+        } else {
+          *reinterpret_cast<f32x4*>(&p.part_o[(seg * G + g) * D + d4 * 4]) = O;
+          if (d4 == 0) {
+            p.part_ml[(seg * G + g) * 2 + 0] = M;
+            p.part_ml[(seg * G + g) * 2 + 1] = L;
+          }
         }
       }
+      // The slot is free again once every read of it above is done.
+      if (lane == 0) {
+        sm_arrive[slot] = 0;
+        __hip_atomic_store(&sm_gen[slot], use + 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
+      }
     }
+    ++piece;
 
     rot = (int)((unsigned)(rot + npairs) % NW);
 
@@ -560,6 +672,8 @@ hipError_t launch_attn_decode(const aflex_attn_args& a, void* ws, hipStream_t st
   const float scale = a.scale != 0.f ? a.scale : 1.0f / sqrtf((float)a.D);
   p.scale_log2 = scale * kLog2e;
   const int P = attn_grid(a, wide);
+  // weighted rounds for the full grid of three 4-wave work-groups per CU
+  p.rounds = (!unit && !wide && a.split_tokens == 0 && P == resident_wgs() && P % 3 == 0) ? 3 : 1;
   const size_t U = (size_t)a.B * a.Hkv;
   const size_t segs = U + (size_t)P;
   const size_t G = (size_t)p.G;
