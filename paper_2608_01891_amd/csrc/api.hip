@@ -584,7 +584,7 @@ aflex_status aflex_af_pipeline_step(const aflex_attn_args* a, const aflex_ffn_ar
       aflex_attn_args am = mb_attn(*a, off, n);
       if (l > 0) am.q = f->y + (size_t)off * H;
       am.out = attn_out + (size_t)off * H;
-      if ((e = aflex::launch_attn_decode(am, attn_ws, sa, true)) != hipSuccess)
+      if ((e = aflex::launch_attn_decode(am, attn_ws, sa, aflex::AttnForm::kWide)) != hipSuccess)
         return hip_status(e, "pipeline: attn");
       if ((e = hipEventRecord(evA[i], sa)) != hipSuccess) return hip_status(e, "pipeline");
       if ((e = hipStreamWaitEvent(sf, evA[i], 0)) != hipSuccess) return hip_status(e, "pipeline");
@@ -665,7 +665,7 @@ aflex_status aflex_af_layer_step(const aflex_attn_args* a, const aflex_ffn_args*
       am.out = attn_out + (size_t)off * HqD;
       // The 4-wave form here: the attention stream also runs o_proj, which
       // shares the CUs better with it than with one 12-wave work-group per CU.
-      if ((e = aflex::launch_attn_decode(am, w + P.attn_ws, sa, false)) != hipSuccess)
+      if ((e = aflex::launch_attn_decode(am, w + P.attn_ws, sa, aflex::AttnForm::kShared)) != hipSuccess)
         return hip_status(e, "layer: attn");
       const uint16_t* res = l > 0 ? f->y + (size_t)off * H : (ly->x_in ? ly->x_in + (size_t)off * H : nullptr);
       const aflex_linear_args lin = mb_linear(*a, *f, *ly, am.out, h + (size_t)off * H, n);

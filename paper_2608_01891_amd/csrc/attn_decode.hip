@@ -12,8 +12,9 @@
 //    charge for the piece it adds; the work-groups take consecutive ranges of
 //    that flattened range in work-group order: equal ones (or a fixed size
 //    the caller asks for), except that in the grid of three work-groups per
-//    CU the three dispatch rounds take ranges weighted 5:3:1, since the
-//    first work-group dispatched to a CU progresses fastest. Every work-group
+//    CU of a call that has the GPU to itself the three dispatch rounds take
+//    ranges weighted 5:3:1, since the first work-group dispatched to a CU
+//    progresses fastest. Every work-group
 //    computes the partition itself from the context lengths (no host
 //    synchronisation, no extra launch); a work-group's range is one or more
 //    pieces, each the part of one unit that falls into it. The grid is the
@@ -650,7 +651,7 @@ size_t attn_workspace_bytes(const aflex_attn_args& a) {
          align_up(U * sizeof(int2), 256);
 }
 
-hipError_t launch_attn_decode(const aflex_attn_args& a, void* ws, hipStream_t stream, bool wide) {
+hipError_t launch_attn_decode(const aflex_attn_args& a, void* ws, hipStream_t stream, AttnForm form) {
   AttnParams p;
   p.q = a.q;
   p.kc = a.k_cache;
@@ -668,12 +669,15 @@ hipError_t launch_attn_decode(const aflex_attn_args& a, void* ws, hipStream_t st
   p.chunk_blocks = a.split_tokens > 0 ? a.split_tokens / 16 : 0;
   p.unit_cost = unit_cost(a);
   const bool unit = unit_per_wg(a);
-  wide = wide && !unit && a.split_tokens == 0;
+  const bool wide = form == AttnForm::kWide && !unit && a.split_tokens == 0;
   const float scale = a.scale != 0.f ? a.scale : 1.0f / sqrtf((float)a.D);
   p.scale_log2 = scale * kLog2e;
   const int P = attn_grid(a, wide);
   // weighted rounds for the full grid of three 4-wave work-groups per CU
-  p.rounds = (!unit && !wide && a.split_tokens == 0 && P == resident_wgs() && P % 3 == 0) ? 3 : 1;
+  // (beside other work the dispatch order no longer places the rounds: the
+  // layer step, whose attention runs beside the MoE stream, took 2.78 ms with
+  // the weighting and 2.75 ms without)
+  p.rounds = (form == AttnForm::kAlone && !unit && a.split_tokens == 0 && P == resident_wgs() && P % 3 == 0) ? 3 : 1;
   const size_t U = (size_t)a.B * a.Hkv;
   const size_t segs = U + (size_t)P;
   const size_t G = (size_t)p.G;

@@ -22,10 +22,15 @@ bool attn_shape_fits(const aflex_attn_args& a);
 size_t attn_workspace_bytes(const aflex_attn_args& a);
 // K/V tiles stream with non-temporal loads: every cached byte is read once,
 // alone and next to the FFN's weight stream in the two-stream step alike
-// (that step: 2.785 -> 2.730 ms against ordinary loads). wide: the even split
-// in one 12-wave work-group per CU, for calls that run beside the FFN's
-// weight stream (the pipeline step); the workspace is the same.
-hipError_t launch_attn_decode(const aflex_attn_args& a, void* ws, hipStream_t stream, bool wide = false);
+// (that step: 2.785 -> 2.730 ms against ordinary loads). The form of the even
+// split: kAlone, three 4-wave work-groups per CU with ranges weighted by
+// dispatch round (the call has the GPU to itself); kWide, one 12-wave
+// work-group per CU (beside the FFN's weight stream, the pipeline step);
+// kShared, three 4-wave work-groups per CU with equal ranges (beside other
+// work that takes CUs first, the layer step). The workspace is the same.
+enum class AttnForm { kAlone, kWide, kShared };
+hipError_t launch_attn_decode(const aflex_attn_args& a, void* ws, hipStream_t stream,
+                              AttnForm form = AttnForm::kAlone);
 
 // Dense SwiGLU FFN (ffn.hip).
 size_t swiglu_workspace_bytes(const aflex_ffn_args& f);
