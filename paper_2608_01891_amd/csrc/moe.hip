@@ -114,6 +114,32 @@ __device__ __forceinline__ void topk_token(const float* l, int E, int k, int* si
   for (int j = 0; j < k; ++j) w[j] = ex[j] / z;
 }
 
+// Copy the logits of `rows` tokens (rows of E floats, contiguous) into LDS rows
+// of stride ls, eight independent loads per lane in flight at a time: the
+// top-k then reads LDS instead of issuing one dependent global load per
+// compared logit (about 16 serial memory round trips per token at E = 8,
+// k = 2).
+__device__ __forceinline__ void stage_logits(const float* __restrict__ src, int rows, int E, int ls, float* s_log,
+                                             int tid) {
+  const int n = rows * E;
+  for (int i0 = 0; i0 < n; i0 += 256 * 8) {
+    float v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int i = i0 + u * 256 + tid;
+      v[u] = i < n ? src[i] : 0.f;
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int i = i0 + u * 256 + tid;
+      if (i < n) {
+        const int r = i / E;
+        s_log[r * ls + (i - r * E)] = v[u];
+      }
+    }
+  }
+}
+
 // m-tiles of bm rows per expert, in expert order (one thread).
 __device__ __forceinline__ void build_tile_map(const int* off, int E, int bm, int32_t* tile_map, int32_t* num_tiles) {
   int nt = 0;
@@ -159,27 +185,36 @@ __global__ __launch_bounds__(256) void moe_route_kernel(const float* __restrict_
   __shared__ int off[kMaxE + 1];
   __shared__ int base[kMaxE];
   __shared__ int wcnt[4][kMaxE];
+  __shared__ float s_log[256 * (kMaxE + 1)];        // one chunk's logits, rows of odd stride
+  __shared__ int s_ids[kSingleRouteMaxT * kMaxK];  // selected experts, read back by step 3
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int ls = E | 1;
   if (tid < kMaxE) {
     cnt[tid] = 0;
     base[tid] = 0;
   }
   __syncthreads();
 
-  // 1. top-k and softmax over the selected logits.
-  for (int t = tid; t < T; t += 256) {
-    int sid[kMaxK];
-    float w[kMaxK];
-    topk_token(logits + (size_t)t * E, E, k, sid, w);
-    for (int j = 0; j < k; ++j) {
-      ids[t * k + j] = sid[j];
-      wts[t * k + j] = w[j];
-      if (u_ids) u_ids[t * k + j] = sid[j];
-      if (u_w) u_w[t * k + j] = w[j];
-      atomicAdd(&cnt[sid[j]], 1);
+  // 1. top-k and softmax over the selected logits, 256 tokens at a time.
+  for (int c0 = 0; c0 < T; c0 += 256) {
+    stage_logits(logits + (size_t)c0 * E, min(256, T - c0), E, ls, s_log, tid);
+    __syncthreads();
+    const int t = c0 + tid;
+    if (t < T) {
+      int sid[kMaxK];
+      float w[kMaxK];
+      topk_token(s_log + tid * ls, E, k, sid, w);
+      for (int j = 0; j < k; ++j) {
+        ids[t * k + j] = sid[j];
+        wts[t * k + j] = w[j];
+        s_ids[t * k + j] = sid[j];
+        if (u_ids) u_ids[t * k + j] = sid[j];
+        if (u_w) u_w[t * k + j] = w[j];
+        atomicAdd(&cnt[sid[j]], 1);
+      }
     }
+    __syncthreads();
   }
-  __syncthreads();
 
   // 2. offsets and the m-tile map.
   if (tid == 0) {
@@ -199,7 +234,7 @@ __global__ __launch_bounds__(256) void moe_route_kernel(const float* __restrict_
     const int t = c0 + tid;
     const bool valid = t < T;
     int my_e[kMaxK], pre[kMaxK];
-    for (int j = 0; j < k; ++j) my_e[j] = valid ? ids[t * k + j] : -1;
+    for (int j = 0; j < k; ++j) my_e[j] = valid ? s_ids[t * k + j] : -1;
     chunk_ranks(my_e, valid, E, k, wave, lane, pre, wcnt);
     __syncthreads();
     if (valid) {
@@ -228,14 +263,18 @@ __global__ __launch_bounds__(256) void moe_topk_kernel(const float* __restrict__
                                                        int32_t* ids, float* wts, int32_t* u_ids, float* u_w,
                                                        int32_t* blockcnt) {
   __shared__ int cnt[kMaxE];
+  __shared__ float s_log[256 * (kMaxE + 1)];
   const int tid = threadIdx.x;
+  const int ls = E | 1;
   if (tid < kMaxE) cnt[tid] = 0;
+  const int t0 = blockIdx.x * 256;
+  stage_logits(logits + (size_t)t0 * E, min(256, T - t0), E, ls, s_log, tid);
   __syncthreads();
-  const int t = blockIdx.x * 256 + tid;
+  const int t = t0 + tid;
   if (t < T) {
     int sid[kMaxK];
     float w[kMaxK];
-    topk_token(logits + (size_t)t * E, E, k, sid, w);
+    topk_token(s_log + tid * ls, E, k, sid, w);
     for (int j = 0; j < k; ++j) {
       ids[t * k + j] = sid[j];
       wts[t * k + j] = w[j];
