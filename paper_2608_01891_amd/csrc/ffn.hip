@@ -22,8 +22,21 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restr
                                                             const uint16_t* __restrict__ residual) {
   const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
   if (i >= n4) return;
-  f32x4 s = *reinterpret_cast<const f32x4*>(P + i * 4);
-  for (int k = 1; k < splits; ++k) s += *reinterpret_cast<const f32x4*>(P + k * split_stride + i * 4);
+  // Four slices are loaded before any is added (indices past the last slice
+  // re-read it and are not added), so a call with many splits waits for one
+  // memory round trip per four slices, not per slice. The sum keeps slice
+  // order and starts from -0, which leaves the first slice's value unchanged.
+  constexpr int kBatch = 4;
+  f32x4 s = {-0.f, -0.f, -0.f, -0.f};
+  for (int k0 = 0; k0 < splits; k0 += kBatch) {
+    f32x4 v[kBatch];
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u)
+      v[u] = *reinterpret_cast<const f32x4*>(P + min(k0 + u, splits - 1) * split_stride + i * 4);
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u)
+      if (k0 + u < splits) s += v[u];
+  }
   if (residual) {  // added after the split sum, before the one rounding
     const ushort4 r = *reinterpret_cast<const ushort4*>(residual + i * 4);
     s[0] += bf2f(r.x);

@@ -340,6 +340,14 @@ __global__ __launch_bounds__(256) void moe_rank_kernel(const int32_t* __restrict
   }
 }
 
+// The loads are issued in two independent batches -- the token's pair
+// positions and weights (and the routed tile count), then the partial rows of
+// up to four splits for all k pairs -- so a token waits for two memory round
+// trips instead of one per pair and per split (inside the two-stream step,
+// where every round trip queues behind the attention stream's loads, the
+// chained form took 44 us per 64-token call on average). Sums keep split order
+// per pair, then pair order.
+template <int KMAX>
 __global__ __launch_bounds__(256) void moe_combine_kernel(const float* __restrict__ P, long long split_stride,
                                                           int splits, int split_slots,
                                                           const int32_t* __restrict__ num_tiles, int n_ntiles,
@@ -350,18 +358,48 @@ __global__ __launch_bounds__(256) void moe_combine_kernel(const float* __restric
   const int t = blockIdx.x;
   const int c = (blockIdx.y * 256 + threadIdx.x) * 4;
   if (c >= H) return;
+  const int routed = split_slots > 0 ? *num_tiles : 0;
+  long long row[KMAX];
+  float wt[KMAX];
+#pragma unroll
+  for (int j = 0; j < KMAX; ++j) {  // pairs past k re-read the last one and are not added
+    const int jj = min(j, k - 1);
+    row[j] = pos[t * k + jj];
+    wt[j] = w[t * k + jj];
+  }
+  // Uses of the loaded values here keep the compiler from sinking these loads
+  // below the split planning, which waits for the routed tile count: all of
+  // them then share one round trip.
+  asm volatile("" ::"s"(routed));
+#pragma unroll
+  for (int j = 0; j < KMAX; ++j) asm volatile("" ::"s"(row[j]), "s"(wt[j]));
   if (split_slots > 0) {  // the down GEMM planned its split count on the device
     int kps;
-    split_plan_slots(*num_tiles * n_ntiles, ksteps, splits, split_slots, &splits, &kps);
+    split_plan_slots(routed * n_ntiles, ksteps, splits, split_slots, &splits, &kps);
+  }
+  // Splits past the last re-read it and are not added; sums start from -0,
+  // which leaves the first split's value unchanged.
+  constexpr int kBatch = 4;
+  f32x4 s[KMAX];
+#pragma unroll
+  for (int j = 0; j < KMAX; ++j) s[j] = f32x4{-0.f, -0.f, -0.f, -0.f};
+  for (int sp0 = 0; sp0 < splits; sp0 += kBatch) {
+    f32x4 v[kBatch][KMAX];
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u)
+#pragma unroll
+      for (int j = 0; j < KMAX; ++j)
+        v[u][j] = *reinterpret_cast<const f32x4*>(P + min(sp0 + u, splits - 1) * split_stride + row[j] * H + c);
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u)
+#pragma unroll
+      for (int j = 0; j < KMAX; ++j)
+        if (sp0 + u < splits) s[j] += v[u][j];
   }
   f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-  for (int j = 0; j < k; ++j) {
-    const long long row = pos[t * k + j];
-    const float wt = w[t * k + j];
-    f32x4 s = *reinterpret_cast<const f32x4*>(P + row * H + c);
-    for (int sp = 1; sp < splits; ++sp) s += *reinterpret_cast<const f32x4*>(P + sp * split_stride + row * H + c);
-    acc += wt * s;
-  }
+#pragma unroll
+  for (int j = 0; j < KMAX; ++j)
+    if (j < k) acc += wt[j] * s[j];
   if (residual) {
     const ushort4 rv = *reinterpret_cast<const ushort4*>(residual + (size_t)t * H + c);
     acc[0] += bf2f(rv.x);
@@ -487,8 +525,13 @@ hipError_t launch_moe_experts(const aflex_ffn_args& f, void* route_ws, void* exp
 
   dim3 grid(f.T, (f.H / 4 + 255) / 256);
   ProfScope ps("moe_combine", stream);
-  moe_combine_kernel<<<grid, 256, 0, stream>>>(P, d.p_split_stride, L.down_splits, d.split_slots, num_tiles,
-                                               d.n_ntiles, f.I / 64, pos, wts, f.k, f.H, residual, f.y);
+  if (f.k <= 2)
+    moe_combine_kernel<2><<<grid, 256, 0, stream>>>(P, d.p_split_stride, L.down_splits, d.split_slots, num_tiles,
+                                                    d.n_ntiles, f.I / 64, pos, wts, f.k, f.H, residual, f.y);
+  else
+    moe_combine_kernel<kMaxK><<<grid, 256, 0, stream>>>(P, d.p_split_stride, L.down_splits, d.split_slots,
+                                                        num_tiles, d.n_ntiles, f.I / 64, pos, wts, f.k, f.H,
+                                                        residual, f.y);
   return hipGetLastError();
 }
 
