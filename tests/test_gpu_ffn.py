@@ -67,3 +67,13 @@ def test_tile_plan_boundaries(gpu_lib, T):
     x, w, _ = synth.custom_ffn(120 + T, T, 320, 640)
     y = aflex.ffn_swiglu(x.to(DEV), w.to(DEV)).cpu()
     check_rows(y, oracle.swiglu_ffn(x, w.w_gate, w.w_up, w.w_down), what=f"swiglu T={T}")
+
+
+@pytest.mark.parametrize("T,H,I", [(8, 128, 7168), (20, 128, 5120)])
+def test_many_down_splits(gpu_lib, T, H, I):
+    """A narrow output and a wide intermediate size split the down GEMM into
+    14 and 10 K slices, which the reduce sums in batches of four (the last
+    batch partly used)."""
+    x, w, _ = synth.custom_ffn(130 + T, T, H, I)
+    y = aflex.ffn_swiglu(x.to(DEV), w.to(DEV)).cpu()
+    check_rows(y, oracle.swiglu_ffn(x, w.w_gate, w.w_up, w.w_down), what=f"swiglu many splits T={T} I={I}")

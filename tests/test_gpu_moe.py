@@ -171,3 +171,17 @@ def test_tile_shape_boundaries(gpu_lib, T):
     y = aflex.moe_ffn(x.to(DEV), w.to(DEV), logits.to(DEV), 2).cpu()
     ref, _, _ = oracle.moe_ffn(x, logits, w.w_gate, w.w_up, w.w_down, 2)
     check_rows(y, ref, what=f"moe tile boundary T={T}")
+
+
+@pytest.mark.parametrize("T,H,I,E,k", [(16, 128, 8192, 4, 3),     # 32-row tiles, 8 splits, k > 2
+                                       (24, 128, 5120, 4, 2),     # 5 splits: a second, partly used batch
+                                       (200, 128, 8192, 2, 2)])   # 256-row tiles, split count planned on the device
+def test_many_down_splits(gpu_lib, T, H, I, E, k):
+    """Narrow H and wide I give the down GEMM many K splits, so the combine sums
+    its partials over more than one batch of four splits (and over k > 2
+    pairs) before weighting them."""
+    x, w, logits = synth.custom_ffn(90 + T, T, H, I, E=E)
+    y, r = aflex.moe_ffn(x.to(DEV), w.to(DEV), logits.to(DEV), k, routing=True)
+    _check_routing(r, logits, k, E)
+    ref, _, _ = oracle.moe_ffn(x, logits, w.w_gate, w.w_up, w.w_down, k)
+    check_rows(y.cpu(), ref, what=f"moe many splits T={T} I={I} k={k}")
